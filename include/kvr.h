@@ -1,0 +1,153 @@
+/*
+ * kvr.h -- C ABI of libkvr: prefill and prefix-reuse continuation attention
+ * for AMD Instinct MI355X (gfx950).
+ *
+ * The operation (paper, Section "Method"): a decoder layer's causal
+ * grouped-query attention in two modes of one computation.
+ *
+ *   prefill   -- L tokens attend causally to each other and their K/V rows
+ *                are written into the layer's cache (Alg. 1: the publisher's
+ *                one-time forward pass that produces the KV artifact).
+ *   continue  -- S new tokens at positions L_prefix .. L_prefix+S-1 attend to
+ *                the cached rows 0 .. L_prefix-1 and causally to their own
+ *                keys (Alg. 2: positions continue from the artifact's length
+ *                and the mask spans the whole cached context).  Claim 1 of the
+ *                paper: row i of a continuation equals row L_prefix+i of a
+ *                prefill of the concatenation, since cached entries of a causal
+ *                prefix never depend on later tokens.
+ *
+ *   For query row at absolute position p, head h, kv head g = h / G with
+ *   G = n_q_heads / n_kv_heads, keys j = 0..p:
+ *       out = sum_j softmax_j(scale * q . k_j) v_j
+ *
+ * Conventions shared by every entry point
+ *   - Tensor pointers are DEVICE pointers owned by the caller; the library
+ *     never allocates, frees or retains device memory and keeps no state
+ *     beyond a per-device properties cache.
+ *   - Layouts are dense row-major:
+ *         Q, out            [tokens][n_q_heads][head_dim]
+ *         K, V (new rows)   [tokens][n_kv_heads][head_dim]
+ *         kcache, vcache    [n_kv_heads][capacity][head_dim]
+ *     Elements are bf16 (KVR_BF16) or fp32 (KVR_F32) as the descriptor says;
+ *     bf16 inputs accumulate in fp32 and the bf16 output is rounded to
+ *     nearest-even.
+ *   - Every call validates all arguments on the host, synchronously, before
+ *     any HIP call; on an error nothing is launched and a kvr_status != 0 is
+ *     returned.  On success the work is enqueued on `stream` (a hipStream_t;
+ *     NULL is the default stream) and the call returns at once.
+ *   - Device pointers must be 16-byte aligned (KVR_ERR_ALIGN otherwise).
+ *   - Zero-length work (L == 0, S == 0, n == 0) is a successful no-op.
+ *   - For a fixed shape and device the results are bitwise reproducible:
+ *     the key split and the order of every reduction are fixed.
+ */
+#ifndef KVR_H
+#define KVR_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define KVR_ABI_VERSION 1
+
+typedef enum {
+    KVR_OK = 0,
+    KVR_ERR_NULL = 1,      /* a required pointer is NULL                          */
+    KVR_ERR_SHAPE = 2,     /* heads, head_dim, lengths or cu_seqlens invalid        */
+    KVR_ERR_DTYPE = 3,     /* unsupported element type                             */
+    KVR_ERR_CAPACITY = 4,  /* the cache rows addressed exceed the capacity         */
+    KVR_ERR_WORKSPACE = 5, /* workspace smaller than kvr_workspace_bytes()         */
+    KVR_ERR_ALIGN = 6,     /* a device pointer is not 16-byte aligned              */
+    KVR_ERR_DEVICE = 7     /* a HIP call or kernel launch failed                   */
+} kvr_status;
+
+typedef enum { KVR_BF16 = 0, KVR_F32 = 1 } kvr_dtype;
+
+/*
+ * Layer descriptor.  The paper's artifact metadata (model id, dtype, length;
+ * Section "Producing an artifact") must match between producer and consumer;
+ * at this level that is the element type and the head geometry, which every
+ * call checks.
+ *   n_q_heads, n_kv_heads  > 0 and n_q_heads % n_kv_heads == 0
+ *   head_dim               64 or 128
+ *   dtype                  a kvr_dtype
+ *   scale                  softmax scale; <= 0 selects 1/sqrt(head_dim)
+ *   capacity               rows per kv head in kcache/vcache (>= 0)
+ */
+typedef struct {
+    int32_t n_q_heads;
+    int32_t n_kv_heads;
+    int32_t head_dim;
+    int32_t dtype;
+    float scale;
+    int32_t reserved; /* must be 0 */
+    int64_t capacity;
+} kvr_desc;
+
+/*
+ * Full causal prefill of L tokens (Alg. 1, attention part).
+ *   Q [L][Hq][d], K/V [L][Hkv][d] in; out [L][Hq][d] out.
+ *   Writes kcache/vcache rows [0, L) of every kv head (exact copies of K/V);
+ *   rows >= L are not touched.  Needs L <= capacity (KVR_ERR_CAPACITY).
+ *   out must not alias Q, K or V.
+ */
+int kvr_prefill(const kvr_desc *desc, const void *Q, const void *K, const void *V, int64_t L,
+                void *out, void *kcache, void *vcache, void *stream);
+
+/*
+ * Continuation of S tokens over a cached prefix (Alg. 2, one forward call).
+ *   Qs [S][Hq][d] at positions L_prefix..L_prefix+S-1; Ks/Vs [S][Hkv][d] are
+ *   their own keys and values; kcache/vcache rows [0, L_prefix) are the
+ *   cached prefix and are only read (many readers may share one cache).
+ *   out [S][Hq][d].  Needs L_prefix <= capacity.  L_prefix == 0 gives a
+ *   prefill of the S tokens (the caches may then be NULL).
+ *   ws: device workspace of at least kvr_workspace_bytes(desc, L_prefix, S, 1)
+ *   bytes (may be NULL when that is 0); it holds per-split partial results.
+ */
+int kvr_continue(const kvr_desc *desc, const void *Qs, const void *Ks, const void *Vs,
+                 const void *kcache, const void *vcache, int64_t L_prefix, int64_t S,
+                 void *out, void *ws, size_t ws_bytes, void *stream);
+
+/*
+ * Many independent continuations of one shared cached prefix (the paper's
+ * N readers of one document), in one call.
+ *   Reader r owns packed rows [cu[r], cu[r+1]) of Qs/Ks/Vs/out, which sit at
+ *   positions L_prefix .. L_prefix + (cu[r+1]-cu[r]) - 1 and see the shared
+ *   prefix plus their own rows causally, never another reader's rows.
+ *   cu_seqlens_host: HOST array of n+1 int32, cu[0] == 0, non-decreasing.
+ *   ws as for kvr_continue with kvr_workspace_bytes(desc, L_prefix, cu[n], n).
+ */
+int kvr_continue_batched(const kvr_desc *desc, const void *Qs, const void *Ks, const void *Vs,
+                         const int32_t *cu_seqlens_host, int32_t n, const void *kcache,
+                         const void *vcache, int64_t L_prefix, void *out, void *ws,
+                         size_t ws_bytes, void *stream);
+
+/*
+ * Cache write: rows [L_cur, L_cur+S) of each kv head receive Ks/Vs
+ * [S][Hkv][d] unchanged (Alg. 2's cache update after a decode step).
+ * Needs 0 <= L_cur and L_cur + S <= capacity.  Other rows are untouched.
+ */
+int kvr_cache_append(const kvr_desc *desc, const void *Ks, const void *Vs, int64_t S,
+                     void *kcache, void *vcache, int64_t L_cur, void *stream);
+
+/*
+ * Workspace bytes a continuation needs: n <= 1 for kvr_continue with
+ * total_S = S, n >= 2 for kvr_continue_batched with total_S = cu[n].
+ * A pure function of its arguments (no device query); returns 0 when no
+ * workspace is needed and (size_t)-1 for an invalid descriptor.
+ */
+size_t kvr_workspace_bytes(const kvr_desc *desc, int64_t L_prefix, int64_t total_S, int32_t n);
+
+/* Static text for a kvr_status value. */
+const char *kvr_strerror(int status);
+
+/* KVR_ABI_VERSION of the loaded library. */
+int kvr_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* KVR_H */

@@ -1,0 +1,269 @@
+// kvr_api.hip -- host side of libkvr: argument validation, work planning
+// (row tiles, key splits, workspace), and kernel launches on the caller's
+// stream.  Validation runs before any HIP call, so every error path can be
+// exercised on a machine without a GPU.
+#include <math.h>
+#include <string.h>
+
+#include "kvr.h"
+#include "kvr_internal.hpp"
+
+namespace kvr {
+namespace {
+
+constexpr int64_t kMaxTokens = (int64_t)1 << 30;   // rows of Q per call; keeps int32 row math safe
+constexpr int64_t kMaxKeys = (int64_t)1 << 40;
+// Split heuristic for the continuation: aim for this many workgroups on the
+// 256-CU part, never split the prefix below this many keys per workgroup.
+constexpr int64_t kTargetWorkgroups = 512;
+constexpr int64_t kMinSplitKeys = 256;
+
+bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
+
+int check_desc(const kvr_desc *d) {
+    if (!d) return KVR_ERR_NULL;
+    if (d->dtype != KVR_BF16 && d->dtype != KVR_F32) return KVR_ERR_DTYPE;
+    if (d->n_q_heads <= 0 || d->n_kv_heads <= 0 || d->n_q_heads % d->n_kv_heads != 0) return KVR_ERR_SHAPE;
+    if (d->n_q_heads > 4096) return KVR_ERR_SHAPE;
+    if (d->head_dim != 64 && d->head_dim != 128) return KVR_ERR_SHAPE;
+    if (d->capacity < 0 || d->capacity > kMaxKeys) return KVR_ERR_SHAPE;
+    if (d->reserved != 0) return KVR_ERR_SHAPE;
+    if (isnan(d->scale) || isinf(d->scale)) return KVR_ERR_SHAPE;
+    return KVR_OK;
+}
+
+float eff_scale(const kvr_desc *d) { return d->scale > 0.f ? d->scale : 1.f / sqrtf((float)d->head_dim); }
+
+int elt_bytes(const kvr_desc *d) { return d->dtype == KVR_BF16 ? 2 : 4; }
+
+int rows_per_tile(const kvr_desc *d) { return d->dtype == KVR_BF16 ? kRowsBf16 : kRowsF32; }
+
+struct Split {
+    int32_t nsplit;
+    int64_t chunk;
+    size_t ws_bytes;
+};
+
+// Key split of a single continuation: enough workgroups to cover the chip,
+// every split a whole number of key tiles.  A pure function of the shape.
+Split plan_split(const kvr_desc *d, int64_t L_prefix, int64_t S) {
+    Split s{1, 0, 0};
+    if (d->dtype != KVR_BF16 || L_prefix <= 0 || S <= 0) return s;
+    const int64_t G = d->n_q_heads / d->n_kv_heads;
+    const int64_t rows = G * S;
+    const int64_t tiles = (rows + kRowsBf16 - 1) / kRowsBf16;
+    const int64_t base = tiles * d->n_kv_heads;
+    if (base >= kTargetWorkgroups) return s;
+    int64_t want = (kTargetWorkgroups + base - 1) / base;
+    const int64_t most = (L_prefix + kMinSplitKeys - 1) / kMinSplitKeys;
+    if (want > most) want = most;
+    if (want <= 1) return s;
+    int64_t chunk = (L_prefix + want - 1) / want;
+    chunk = (chunk + kKeyTile - 1) / kKeyTile * kKeyTile;
+    const int64_t n = (L_prefix + chunk - 1) / chunk;
+    if (n <= 1) return s;
+    s.nsplit = (int32_t)n;
+    s.chunk = chunk;
+    s.ws_bytes = (size_t)n * d->n_kv_heads * rows * (d->head_dim + 2) * sizeof(float);
+    return s;
+}
+
+int to_status(hipError_t e) { return e == hipSuccess ? KVR_OK : KVR_ERR_DEVICE; }
+
+void fill_common(AttnParams &p, const kvr_desc *d) {
+    memset(&p, 0, sizeof p);
+    p.n_q_heads = d->n_q_heads;
+    p.n_kv_heads = d->n_kv_heads;
+    p.group = d->n_q_heads / d->n_kv_heads;
+    p.scale = eff_scale(d);
+    p.scale_log2 = p.scale * 1.4426950408889634f;
+    p.cap = d->capacity;
+    p.nsplit = 1;
+}
+
+// One segment: rows of tokens [0, n_tok).
+int launch_single(const kvr_desc *d, const void *Q, const void *K, const void *V, const void *kc,
+                  const void *vc, int64_t n_prefix, int64_t n_tok, void *out, const Split &sp, void *ws,
+                  bool reverse, hipStream_t stream) {
+    AttnParams p;
+    fill_common(p, d);
+    p.q = Q; p.kn = K; p.vn = V; p.kc = kc; p.vc = vc; p.out = out;
+    p.ws = (float *)ws;
+    p.n_prefix = n_prefix;
+    p.nsplit = sp.nsplit;
+    p.chunk = sp.chunk;
+    const int64_t G = p.group;
+    const int64_t rows = G * n_tok;
+    if (rows > 0x7fffffff) return KVR_ERR_SHAPE;   // row indices are 32-bit on the device
+    const int rpt = rows_per_tile(d);
+    const int64_t tiles = (rows + rpt - 1) / rpt;
+    p.n_seg = 1;
+    p.reverse = reverse ? 1 : 0;
+    p.tiles_total = (int32_t)tiles;
+    p.rows_total = (int32_t)rows;
+    p.seg_tok0[0] = 0;
+    p.seg_tok0[1] = (int32_t)n_tok;
+    p.seg_tile0[0] = 0;
+    p.seg_tile0[1] = (int32_t)tiles;
+    const int64_t grid = tiles * p.nsplit * p.n_kv_heads;
+    if (grid <= 0) return KVR_OK;
+    if (grid > 0x7fffffff) return KVR_ERR_SHAPE;
+    hipError_t e = d->dtype == KVR_BF16 ? launch_attn_bf16(p, d->head_dim, (int)grid, stream)
+                                        : launch_attn_f32(p, d->head_dim, (int)grid, stream);
+    if (e != hipSuccess) return KVR_ERR_DEVICE;
+    if (p.nsplit > 1) {
+        MergeParams m;
+        m.ws = p.ws; m.out = out; m.nsplit = p.nsplit; m.n_q_heads = p.n_q_heads;
+        m.n_kv_heads = p.n_kv_heads; m.group = p.group; m.rows = (int32_t)rows;
+        e = launch_merge_bf16(m, d->head_dim, stream);
+        if (e != hipSuccess) return KVR_ERR_DEVICE;
+    }
+    return KVR_OK;
+}
+
+int append_impl(const kvr_desc *d, const void *Ks, const void *Vs, int64_t S, void *kc, void *vc,
+                int64_t L_cur, hipStream_t stream) {
+    AppendParams a;
+    a.k = Ks; a.v = Vs; a.kc = kc; a.vc = vc;
+    a.S = S; a.L_cur = L_cur; a.cap = d->capacity;
+    a.n_kv_heads = d->n_kv_heads;
+    a.row_chunks = d->head_dim * elt_bytes(d) / 16;
+    return to_status(launch_append(a, stream));
+}
+
+}  // namespace
+}  // namespace kvr
+
+using namespace kvr;
+
+extern "C" {
+
+int kvr_abi_version(void) { return KVR_ABI_VERSION; }
+
+const char *kvr_strerror(int status) {
+    switch (status) {
+        case KVR_OK: return "ok";
+        case KVR_ERR_NULL: return "a required pointer is NULL";
+        case KVR_ERR_SHAPE: return "invalid heads, head_dim, length or cu_seqlens";
+        case KVR_ERR_DTYPE: return "unsupported element type";
+        case KVR_ERR_CAPACITY: return "cache rows exceed the descriptor's capacity";
+        case KVR_ERR_WORKSPACE: return "workspace smaller than kvr_workspace_bytes()";
+        case KVR_ERR_ALIGN: return "device pointer not 16-byte aligned";
+        case KVR_ERR_DEVICE: return "HIP call or kernel launch failed";
+        default: return "unknown kvr status";
+    }
+}
+
+size_t kvr_workspace_bytes(const kvr_desc *desc, int64_t L_prefix, int64_t total_S, int32_t n) {
+    if (check_desc(desc) != KVR_OK || L_prefix < 0 || total_S < 0 || n < 0) return (size_t)-1;
+    if (n >= 2) return 0;   // many readers: no key split, one workgroup per (reader tile, kv head)
+    return plan_split(desc, L_prefix, total_S).ws_bytes;
+}
+
+int kvr_prefill(const kvr_desc *desc, const void *Q, const void *K, const void *V, int64_t L, void *out,
+                void *kcache, void *vcache, void *stream) {
+    int st = check_desc(desc);
+    if (st) return st;
+    if (L < 0 || L > kMaxTokens) return KVR_ERR_SHAPE;
+    if (L > desc->capacity) return KVR_ERR_CAPACITY;
+    if (L == 0) return KVR_OK;
+    if (!Q || !K || !V || !out || !kcache || !vcache) return KVR_ERR_NULL;
+    if (!aligned16(Q) || !aligned16(K) || !aligned16(V) || !aligned16(out) || !aligned16(kcache) ||
+        !aligned16(vcache))
+        return KVR_ERR_ALIGN;
+    hipStream_t s = (hipStream_t)stream;
+    st = append_impl(desc, K, V, L, kcache, vcache, 0, s);
+    if (st) return st;
+    Split none{1, 0, 0};
+    return launch_single(desc, Q, K, V, nullptr, nullptr, 0, L, out, none, nullptr, true, s);
+}
+
+int kvr_continue(const kvr_desc *desc, const void *Qs, const void *Ks, const void *Vs, const void *kcache,
+                 const void *vcache, int64_t L_prefix, int64_t S, void *out, void *ws, size_t ws_bytes,
+                 void *stream) {
+    int st = check_desc(desc);
+    if (st) return st;
+    if (L_prefix < 0 || S < 0 || S > kMaxTokens || L_prefix > kMaxKeys) return KVR_ERR_SHAPE;
+    if (L_prefix > desc->capacity) return KVR_ERR_CAPACITY;
+    if (S == 0) return KVR_OK;
+    if (!Qs || !Ks || !Vs || !out) return KVR_ERR_NULL;
+    if (L_prefix > 0 && (!kcache || !vcache)) return KVR_ERR_NULL;
+    const Split sp = plan_split(desc, L_prefix, S);
+    if (ws_bytes < sp.ws_bytes) return KVR_ERR_WORKSPACE;
+    if (sp.ws_bytes > 0 && !ws) return KVR_ERR_NULL;
+    if (!aligned16(Qs) || !aligned16(Ks) || !aligned16(Vs) || !aligned16(out) || !aligned16(kcache) ||
+        !aligned16(vcache) || !aligned16(ws))
+        return KVR_ERR_ALIGN;
+    return launch_single(desc, Qs, Ks, Vs, kcache, vcache, L_prefix, S, out, sp, ws, false,
+                         (hipStream_t)stream);
+}
+
+int kvr_continue_batched(const kvr_desc *desc, const void *Qs, const void *Ks, const void *Vs,
+                         const int32_t *cu, int32_t n, const void *kcache, const void *vcache,
+                         int64_t L_prefix, void *out, void *ws, size_t ws_bytes, void *stream) {
+    (void)ws; (void)ws_bytes;   // the batched path needs no workspace
+    int st = check_desc(desc);
+    if (st) return st;
+    if (n < 0 || L_prefix < 0 || L_prefix > kMaxKeys) return KVR_ERR_SHAPE;
+    if (L_prefix > desc->capacity) return KVR_ERR_CAPACITY;
+    if (n == 0) return KVR_OK;
+    if (!cu) return KVR_ERR_NULL;
+    if (cu[0] != 0) return KVR_ERR_SHAPE;
+    for (int32_t i = 0; i < n; ++i)
+        if (cu[i + 1] < cu[i]) return KVR_ERR_SHAPE;
+    const int64_t total = cu[n];
+    if (total > kMaxTokens) return KVR_ERR_SHAPE;
+    for (int32_t i = 0; i < n; ++i)
+        if ((int64_t)(desc->n_q_heads / desc->n_kv_heads) * (cu[i + 1] - cu[i]) > 0x7fffffff) return KVR_ERR_SHAPE;
+    if (total == 0) return KVR_OK;
+    if (!Qs || !Ks || !Vs || !out) return KVR_ERR_NULL;
+    if (L_prefix > 0 && (!kcache || !vcache)) return KVR_ERR_NULL;
+    if (!aligned16(Qs) || !aligned16(Ks) || !aligned16(Vs) || !aligned16(out) || !aligned16(kcache) ||
+        !aligned16(vcache))
+        return KVR_ERR_ALIGN;
+
+    const int64_t G = desc->n_q_heads / desc->n_kv_heads;
+    const int rpt = rows_per_tile(desc);
+    for (int32_t first = 0; first < n; first += kMaxSegments) {
+        const int32_t cnt = (n - first) < kMaxSegments ? (n - first) : kMaxSegments;
+        AttnParams p;
+        fill_common(p, desc);
+        p.q = Qs; p.kn = Ks; p.vn = Vs; p.kc = kcache; p.vc = vcache; p.out = out;
+        p.n_prefix = L_prefix;
+        p.reverse = 0;
+        int32_t tiles = 0, seg = 0;
+        for (int32_t i = 0; i < cnt; ++i) {
+            const int64_t len = cu[first + i + 1] - cu[first + i];
+            if (len == 0) continue;   // an empty reader has no rows
+            p.seg_tok0[seg] = cu[first + i];
+            p.seg_tok0[seg + 1] = cu[first + i + 1];
+            p.seg_tile0[seg] = tiles;
+            tiles += (int32_t)((G * len + rpt - 1) / rpt);
+            ++seg;
+        }
+        if (seg == 0) continue;
+        p.seg_tile0[seg] = tiles;
+        p.n_seg = seg;
+        p.tiles_total = tiles;
+        p.rows_total = 0;
+        const int64_t grid = (int64_t)tiles * p.n_kv_heads;
+        hipError_t e = desc->dtype == KVR_BF16 ? launch_attn_bf16(p, desc->head_dim, (int)grid, (hipStream_t)stream)
+                                               : launch_attn_f32(p, desc->head_dim, (int)grid, (hipStream_t)stream);
+        if (e != hipSuccess) return KVR_ERR_DEVICE;
+    }
+    return KVR_OK;
+}
+
+int kvr_cache_append(const kvr_desc *desc, const void *Ks, const void *Vs, int64_t S, void *kcache,
+                     void *vcache, int64_t L_cur, void *stream) {
+    int st = check_desc(desc);
+    if (st) return st;
+    if (S < 0 || L_cur < 0 || S > kMaxTokens || L_cur > kMaxKeys) return KVR_ERR_SHAPE;
+    if (L_cur + S > desc->capacity) return KVR_ERR_CAPACITY;
+    if (S == 0) return KVR_OK;
+    if (!Ks || !Vs || !kcache || !vcache) return KVR_ERR_NULL;
+    if (!aligned16(Ks) || !aligned16(Vs) || !aligned16(kcache) || !aligned16(vcache)) return KVR_ERR_ALIGN;
+    return append_impl(desc, Ks, Vs, S, kcache, vcache, L_cur, (hipStream_t)stream);
+}
+
+}  // extern "C"

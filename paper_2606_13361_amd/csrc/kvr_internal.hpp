@@ -1,0 +1,69 @@
+// kvr_internal.hpp -- launch parameters shared by the host entry points and
+// the gfx950 kernels of libkvr.  Not part of the public ABI (include/kvr.h).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace kvr {
+
+// Readers handled by one launch of the attention kernel; kvr_continue_batched
+// issues one launch per group of this many readers.
+constexpr int kMaxSegments = 128;
+
+// Query rows are (token, head) pairs packed token-major: for kv head g with
+// group size G, row r of a segment is token r / G, query head g*G + r % G.
+// That keeps every row of a workgroup on the same K/V rows.
+struct AttnParams {
+    const void *q;   // [tokens][n_q_heads][D]
+    const void *kn;  // new keys   [tokens][n_kv_heads][D]
+    const void *vn;  // new values [tokens][n_kv_heads][D]
+    const void *kc;  // cached keys   [n_kv_heads][cap][D]
+    const void *vc;  // cached values [n_kv_heads][cap][D]
+    void *out;       // [tokens][n_q_heads][D]
+    float *ws;       // split partials: O [nsplit][Hkv][rows][D], then (m, l) [nsplit][Hkv][rows][2]
+    int64_t cap;
+    int64_t n_prefix;  // cached keys, positions [0, n_prefix); every query row sees them all
+    int64_t chunk;     // prefix keys per split, a multiple of the key tile
+    int32_t n_q_heads, n_kv_heads, group;
+    int32_t nsplit;
+    float scale;        // softmax scale
+    float scale_log2;   // scale * log2(e)
+    int32_t n_seg;      // segments (independent readers); 1 for prefill / continue
+    int32_t reverse;    // visit row tiles last-first (longest causal rows first)
+    int32_t tiles_total;
+    int32_t rows_total;  // rows per kv head (partials indexing, single segment)
+    int32_t seg_tok0[kMaxSegments + 1];   // packed token offset of each segment (cu_seqlens)
+    int32_t seg_tile0[kMaxSegments + 1];  // first row tile of each segment (prefix sums)
+};
+
+struct AppendParams {
+    const void *k;  // [S][n_kv_heads][D]
+    const void *v;
+    void *kc;       // [n_kv_heads][cap][D]
+    void *vc;
+    int64_t S, L_cur, cap;
+    int32_t n_kv_heads;
+    int32_t row_chunks;  // 16-byte chunks per row (D * elt / 16)
+};
+
+struct MergeParams {
+    const float *ws;
+    void *out;
+    int32_t nsplit, n_q_heads, n_kv_heads, group, rows;
+};
+
+// bf16 path (MFMA), D in {64, 128}
+hipError_t launch_attn_bf16(const AttnParams &p, int head_dim, int grid, hipStream_t s);
+hipError_t launch_merge_bf16(const MergeParams &p, int head_dim, hipStream_t s);
+// fp32 path (VALU), D in {64, 128}
+hipError_t launch_attn_f32(const AttnParams &p, int head_dim, int grid, hipStream_t s);
+// cache write
+hipError_t launch_append(const AppendParams &p, hipStream_t s);
+
+// row-tile geometry of the two paths
+constexpr int kRowsBf16 = 128;  // query rows per workgroup, bf16 path
+constexpr int kRowsF32 = 64;    // query rows per workgroup, fp32 path
+constexpr int kKeyTile = 64;    // keys per tile (split chunks are multiples of it)
+
+}  // namespace kvr

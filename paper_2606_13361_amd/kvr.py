@@ -1,0 +1,194 @@
+"""Python binding of libkvr (include/kvr.h): argument marshalling only.
+
+Every function has the name of the C entry point it calls.  Tensors are torch
+tensors on the GPU (PyTorch provides device memory and streams); their
+dtype, device, contiguity and shape are checked against the layer descriptor
+before the call -- the consumer-side metadata check of the paper's Alg. 2 --
+and a ValueError is raised on a mismatch.  A nonzero kvr_status raises
+KvrError.  There is no fallback: without the built library every call fails.
+"""
+import ctypes
+import os
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libkvr.so")
+
+KVR_OK, KVR_ERR_NULL, KVR_ERR_SHAPE, KVR_ERR_DTYPE = 0, 1, 2, 3
+KVR_ERR_CAPACITY, KVR_ERR_WORKSPACE, KVR_ERR_ALIGN, KVR_ERR_DEVICE = 4, 5, 6, 7
+KVR_BF16, KVR_F32 = 0, 1
+
+EXPORTS = ("kvr_prefill", "kvr_continue", "kvr_continue_batched", "kvr_cache_append",
+           "kvr_workspace_bytes", "kvr_strerror", "kvr_abi_version")
+
+_TORCH_DTYPE = {KVR_BF16: torch.bfloat16, KVR_F32: torch.float32}
+
+
+class kvr_desc(ctypes.Structure):
+    _fields_ = [("n_q_heads", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("dtype", ctypes.c_int32),
+                ("scale", ctypes.c_float), ("reserved", ctypes.c_int32),
+                ("capacity", ctypes.c_int64)]
+
+
+class KvrError(RuntimeError):
+    def __init__(self, status, where):
+        self.status = status
+        super().__init__("%s: %s (status %d)" % (where, strerror(status), status))
+
+
+_lib = None
+
+
+def load():
+    """Load the in-tree libkvr.so; raise if it was not built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError("libkvr.so is not built (run __graft_entry__.build() or "
+                           "python -m paper_2606_13361_amd.build)")
+    lib = ctypes.CDLL(LIB_PATH)
+    P, I64, SZ = ctypes.c_void_p, ctypes.c_int64, ctypes.c_size_t
+    D = ctypes.POINTER(kvr_desc)
+    lib.kvr_prefill.argtypes = [D, P, P, P, I64, P, P, P, P]
+    lib.kvr_continue.argtypes = [D, P, P, P, P, P, I64, I64, P, P, SZ, P]
+    lib.kvr_continue_batched.argtypes = [D, P, P, P, ctypes.POINTER(ctypes.c_int32), ctypes.c_int32,
+                                         P, P, I64, P, P, SZ, P]
+    lib.kvr_cache_append.argtypes = [D, P, P, I64, P, P, I64, P]
+    lib.kvr_workspace_bytes.argtypes = [D, I64, I64, ctypes.c_int32]
+    lib.kvr_workspace_bytes.restype = SZ
+    lib.kvr_strerror.argtypes = [ctypes.c_int]
+    lib.kvr_strerror.restype = ctypes.c_char_p
+    lib.kvr_abi_version.argtypes = []
+    for f in (lib.kvr_prefill, lib.kvr_continue, lib.kvr_continue_batched, lib.kvr_cache_append,
+              lib.kvr_abi_version):
+        f.restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def strerror(status):
+    return load().kvr_strerror(int(status)).decode()
+
+
+def kvr_abi_version():
+    return load().kvr_abi_version()
+
+
+def make_desc(n_q_heads, n_kv_heads, head_dim, dtype, capacity, scale=0.0):
+    """dtype: torch.bfloat16 / torch.float32 or KVR_BF16 / KVR_F32."""
+    if isinstance(dtype, torch.dtype):
+        dtype = {torch.bfloat16: KVR_BF16, torch.float32: KVR_F32}.get(dtype, -1)
+    return kvr_desc(int(n_q_heads), int(n_kv_heads), int(head_dim), int(dtype), float(scale), 0,
+                    int(capacity))
+
+
+def _stream(stream):
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, torch.cuda.Stream):
+        return stream.cuda_stream
+    return int(stream)
+
+
+def _check(t, name, desc, shape):
+    if not isinstance(t, torch.Tensor):
+        raise ValueError("%s must be a torch tensor" % name)
+    if not t.is_cuda:
+        raise ValueError("%s must be on the GPU" % name)
+    want = _TORCH_DTYPE.get(desc.dtype)
+    if t.dtype != want:
+        raise ValueError("%s has dtype %s, the layer descriptor says %s" % (name, t.dtype, want))
+    if not t.is_contiguous():
+        raise ValueError("%s must be contiguous" % name)
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError("%s has shape %s, expected %s" % (name, tuple(t.shape), tuple(shape)))
+    return t.data_ptr()
+
+
+def _cache_ptrs(desc, kcache, vcache, required):
+    if kcache is None and vcache is None and not required:
+        return None, None
+    shape = (desc.n_kv_heads, desc.capacity, desc.head_dim)
+    return _check(kcache, "kcache", desc, shape), _check(vcache, "vcache", desc, shape)
+
+
+def _raise(st, where):
+    if st != KVR_OK:
+        raise KvrError(st, where)
+
+
+def kvr_workspace_bytes(desc, L_prefix, total_S, n=1):
+    return load().kvr_workspace_bytes(ctypes.byref(desc), int(L_prefix), int(total_S), int(n))
+
+
+def kvr_prefill(desc, Q, K, V, L, out, kcache, vcache, stream=None):
+    Hq, Hkv, d = desc.n_q_heads, desc.n_kv_heads, desc.head_dim
+    q = _check(Q, "Q", desc, (L, Hq, d))
+    k = _check(K, "K", desc, (L, Hkv, d))
+    v = _check(V, "V", desc, (L, Hkv, d))
+    o = _check(out, "out", desc, (L, Hq, d))
+    kc, vc = _cache_ptrs(desc, kcache, vcache, True)
+    _raise(load().kvr_prefill(ctypes.byref(desc), q, k, v, int(L), o, kc, vc, _stream(stream)),
+           "kvr_prefill")
+
+
+def kvr_continue(desc, Qs, Ks, Vs, kcache, vcache, L_prefix, S, out, ws=None, stream=None):
+    Hq, Hkv, d = desc.n_q_heads, desc.n_kv_heads, desc.head_dim
+    q = _check(Qs, "Qs", desc, (S, Hq, d))
+    k = _check(Ks, "Ks", desc, (S, Hkv, d))
+    v = _check(Vs, "Vs", desc, (S, Hkv, d))
+    o = _check(out, "out", desc, (S, Hq, d))
+    kc, vc = _cache_ptrs(desc, kcache, vcache, L_prefix > 0)
+    wp, wn = _workspace(ws)
+    _raise(load().kvr_continue(ctypes.byref(desc), q, k, v, kc, vc, int(L_prefix), int(S), o, wp, wn,
+                               _stream(stream)), "kvr_continue")
+
+
+def kvr_continue_batched(desc, Qs, Ks, Vs, cu_seqlens, kcache, vcache, L_prefix, out, ws=None,
+                         stream=None):
+    """cu_seqlens: host sequence of n+1 ints (a list or a CPU tensor)."""
+    Hq, Hkv, d = desc.n_q_heads, desc.n_kv_heads, desc.head_dim
+    cu = [int(x) for x in (cu_seqlens.tolist() if isinstance(cu_seqlens, torch.Tensor) else cu_seqlens)]
+    n = len(cu) - 1
+    if n < 0:
+        raise ValueError("cu_seqlens needs at least one entry")
+    total = cu[-1]
+    q = _check(Qs, "Qs", desc, (total, Hq, d))
+    k = _check(Ks, "Ks", desc, (total, Hkv, d))
+    v = _check(Vs, "Vs", desc, (total, Hkv, d))
+    o = _check(out, "out", desc, (total, Hq, d))
+    kc, vc = _cache_ptrs(desc, kcache, vcache, L_prefix > 0)
+    arr = (ctypes.c_int32 * len(cu))(*cu)
+    wp, wn = _workspace(ws)
+    _raise(load().kvr_continue_batched(ctypes.byref(desc), q, k, v, arr, n, kc, vc, int(L_prefix), o,
+                                       wp, wn, _stream(stream)), "kvr_continue_batched")
+
+
+def kvr_cache_append(desc, Ks, Vs, S, kcache, vcache, L_cur, stream=None):
+    Hkv, d = desc.n_kv_heads, desc.head_dim
+    k = _check(Ks, "Ks", desc, (S, Hkv, d))
+    v = _check(Vs, "Vs", desc, (S, Hkv, d))
+    kc, vc = _cache_ptrs(desc, kcache, vcache, True)
+    _raise(load().kvr_cache_append(ctypes.byref(desc), k, v, int(S), kc, vc, int(L_cur), _stream(stream)),
+           "kvr_cache_append")
+
+
+def _workspace(ws):
+    if ws is None:
+        return None, 0
+    if not isinstance(ws, torch.Tensor) or not ws.is_cuda or not ws.is_contiguous():
+        raise ValueError("ws must be a contiguous GPU tensor")
+    return ws.data_ptr(), ws.numel() * ws.element_size()
+
+
+def workspace_for(desc, L_prefix, total_S, n=1, device="cuda"):
+    """Allocate (with torch) the workspace a continuation needs, or None."""
+    nb = kvr_workspace_bytes(desc, L_prefix, total_S, n)
+    if nb == ctypes.c_size_t(-1).value:
+        raise ValueError("invalid layer descriptor")
+    if nb == 0:
+        return None
+    return torch.empty(nb, dtype=torch.uint8, device=device)

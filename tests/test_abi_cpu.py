@@ -1,0 +1,198 @@
+"""The C ABI without a GPU: the library loads, exports what include/kvr.h
+declares, and rejects every invalid argument on the host before any HIP call.
+
+Pointers here are fake integers (never dereferenced): validation returns
+before any launch, so no device is touched.
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2606_13361_amd import kvr
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "kvr.h")
+
+A = 0x1000          # a 16-byte-aligned fake device pointer
+MIS = 0x1008        # 8-byte aligned only
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(kvr.LIB_PATH):
+        from paper_2606_13361_amd import build
+        build.build()
+    return kvr.load()
+
+
+def desc(**kw):
+    d = dict(n_q_heads=32, n_kv_heads=8, head_dim=128, dtype=kvr.KVR_BF16, capacity=4096, scale=0.0)
+    d.update(kw)
+    return kvr.make_desc(d["n_q_heads"], d["n_kv_heads"], d["head_dim"], d["dtype"], d["capacity"], d["scale"])
+
+
+def header_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(kvr_[a-z_]+)\s*\(", text)))
+
+
+def exported_symbols(path):
+    """Dynamic symbol names of the shared library, read from its ELF tables."""
+    import struct
+    data = open(path, "rb").read()
+    assert data[:4] == b"\x7fELF" and data[4] == 2    # 64-bit
+    shoff, = struct.unpack_from("<Q", data, 0x28)
+    shentsize, shnum, _ = struct.unpack_from("<HHH", data, 0x3A)
+    secs = [struct.unpack_from("<IIQQQQIIQQ", data, shoff + i * shentsize) for i in range(shnum)]
+    names = set()
+    for s in secs:
+        if s[1] == 11:                         # SHT_DYNSYM
+            strtab = secs[s[6]]
+            off, size, ent = s[4], s[5], s[9]
+            for k in range(size // ent):
+                st_name, st_info, _, st_shndx, _, _ = struct.unpack_from("<IBBHQQ", data, off + k * ent)
+                if st_shndx != 0 and (st_info >> 4) == 1:   # defined, global
+                    nm = data[strtab[4] + st_name: data.index(b"\0", strtab[4] + st_name)]
+                    names.add(nm.decode())
+    return names
+
+
+def test_exports_match_header(lib):
+    declared = header_functions()
+    assert set(declared) == set(kvr.EXPORTS)
+    syms = exported_symbols(kvr.LIB_PATH)
+    for name in declared:
+        assert name in syms, name
+        assert hasattr(lib, name)
+
+
+def test_abi_version_and_strerror(lib):
+    assert lib.kvr_abi_version() == 1
+    for code in range(8):
+        assert len(lib.kvr_strerror(code)) > 0
+    assert b"unknown" in lib.kvr_strerror(99)
+
+
+def prefill(lib, d, L=16, Q=A, K=A, V=A, out=A, kc=A, vc=A):
+    return lib.kvr_prefill(ctypes.byref(d), Q, K, V, L, out, kc, vc, None)
+
+
+def cont(lib, d, Lp=64, S=8, Q=A, K=A, V=A, kc=A, vc=A, out=A, ws=A, wsb=1 << 30):
+    return lib.kvr_continue(ctypes.byref(d), Q, K, V, kc, vc, Lp, S, out, ws, wsb, None)
+
+
+def append(lib, d, S=4, Lc=0, K=A, V=A, kc=A, vc=A):
+    return lib.kvr_cache_append(ctypes.byref(d), K, V, S, kc, vc, Lc, None)
+
+
+def batched(lib, d, cu, Lp=64, Q=A, K=A, V=A, kc=A, vc=A, out=A):
+    arr = (ctypes.c_int32 * len(cu))(*cu)
+    return lib.kvr_continue_batched(ctypes.byref(d), Q, K, V, arr, len(cu) - 1, kc, vc, Lp, out, None, 0, None)
+
+
+@pytest.mark.parametrize("bad,code", [
+    (dict(n_q_heads=30, n_kv_heads=8), kvr.KVR_ERR_SHAPE),   # Hq % Hkv != 0
+    (dict(n_q_heads=0), kvr.KVR_ERR_SHAPE),
+    (dict(n_kv_heads=0), kvr.KVR_ERR_SHAPE),
+    (dict(head_dim=96), kvr.KVR_ERR_SHAPE),
+    (dict(head_dim=256), kvr.KVR_ERR_SHAPE),
+    (dict(dtype=7), kvr.KVR_ERR_DTYPE),
+    (dict(capacity=-1), kvr.KVR_ERR_SHAPE),
+    (dict(scale=float("nan")), kvr.KVR_ERR_SHAPE),
+])
+def test_descriptor_errors(lib, bad, code):
+    d = desc(**bad)
+    assert prefill(lib, d) == code
+    assert cont(lib, d) == code
+    assert append(lib, d) == code
+    assert batched(lib, d, [0, 4]) == code
+    assert lib.kvr_workspace_bytes(ctypes.byref(d), 64, 8, 1) == ctypes.c_size_t(-1).value
+
+
+def test_null_descriptor(lib):
+    assert lib.kvr_prefill(None, A, A, A, 4, A, A, A, None) == kvr.KVR_ERR_NULL
+    assert lib.kvr_cache_append(None, A, A, 4, A, A, 0, None) == kvr.KVR_ERR_NULL
+
+
+def test_reserved_field_must_be_zero(lib):
+    d = desc()
+    d.reserved = 1
+    assert prefill(lib, d) == kvr.KVR_ERR_SHAPE
+
+
+def test_prefill_errors(lib):
+    d = desc(capacity=100)
+    assert prefill(lib, d, L=-1) == kvr.KVR_ERR_SHAPE
+    assert prefill(lib, d, L=101) == kvr.KVR_ERR_CAPACITY
+    assert prefill(lib, d, L=0, Q=None, K=None, V=None, out=None, kc=None, vc=None) == kvr.KVR_OK
+    for kw in ("Q", "K", "V", "out", "kc", "vc"):
+        assert prefill(lib, d, **{kw: None}) == kvr.KVR_ERR_NULL, kw
+        assert prefill(lib, d, **{kw: MIS}) == kvr.KVR_ERR_ALIGN, kw
+
+
+def test_continue_errors(lib):
+    d = desc(capacity=100)
+    assert cont(lib, d, Lp=-1) == kvr.KVR_ERR_SHAPE
+    assert cont(lib, d, S=-2) == kvr.KVR_ERR_SHAPE
+    assert cont(lib, d, Lp=101) == kvr.KVR_ERR_CAPACITY
+    assert cont(lib, d, S=0, Q=None, K=None, V=None, out=None) == kvr.KVR_OK
+    for kw in ("Q", "K", "V", "out", "kc", "vc"):
+        assert cont(lib, d, **{kw: None}) == kvr.KVR_ERR_NULL, kw
+        assert cont(lib, d, **{kw: MIS}) == kvr.KVR_ERR_ALIGN, kw
+
+
+def test_continue_workspace(lib):
+    d = desc(capacity=8192)
+    need = lib.kvr_workspace_bytes(ctypes.byref(d), 4096, 24, 1)
+    assert need > 0
+    assert cont(lib, d, Lp=4096, S=24, wsb=need - 1) == kvr.KVR_ERR_WORKSPACE
+    assert cont(lib, d, Lp=4096, S=24, ws=None, wsb=need) == kvr.KVR_ERR_NULL
+    assert cont(lib, d, Lp=4096, S=24, ws=MIS, wsb=need) == kvr.KVR_ERR_ALIGN
+
+
+def test_workspace_bytes_is_a_pure_plan(lib):
+    d = desc(capacity=1 << 16)
+    f = lambda Lp, S, n=1, dd=d: lib.kvr_workspace_bytes(ctypes.byref(dd), Lp, S, n)
+    assert f(0, 24) == 0                       # nothing cached: no split
+    assert f(100, 24) == 0                     # short prefix: one split
+    assert f(32768, 24) > f(4096, 24) > 0      # longer prefix: more splits
+    assert f(32768, 24) == f(32768, 24)        # deterministic
+    assert f(32768, 24, 64) == 0               # many readers: never split
+    assert f(32768, 1) % (8 * 4 * (128 + 2) * 4) == 0   # whole partial rows of fp32
+    assert f(32768, 24, 1, desc(dtype=kvr.KVR_F32, capacity=1 << 16)) == 0
+    assert f(-1, 3) == ctypes.c_size_t(-1).value
+
+
+def test_append_errors(lib):
+    d = desc(capacity=50)
+    assert append(lib, d, S=-1) == kvr.KVR_ERR_SHAPE
+    assert append(lib, d, Lc=-1) == kvr.KVR_ERR_SHAPE
+    assert append(lib, d, S=10, Lc=41) == kvr.KVR_ERR_CAPACITY
+    assert append(lib, d, S=0, K=None, V=None, kc=None, vc=None) == kvr.KVR_OK
+    for kw in ("K", "V", "kc", "vc"):
+        assert append(lib, d, **{kw: None}) == kvr.KVR_ERR_NULL
+        assert append(lib, d, **{kw: MIS}) == kvr.KVR_ERR_ALIGN
+
+
+def test_batched_errors(lib):
+    d = desc(capacity=100)
+    assert batched(lib, d, [1, 4]) == kvr.KVR_ERR_SHAPE       # cu[0] != 0
+    assert batched(lib, d, [0, 4, 3]) == kvr.KVR_ERR_SHAPE    # decreasing
+    assert batched(lib, d, [0, 4], Lp=101) == kvr.KVR_ERR_CAPACITY
+    assert batched(lib, d, [0]) == kvr.KVR_OK                  # no readers
+    assert batched(lib, d, [0, 0, 0], Q=None) == kvr.KVR_OK    # only empty readers
+    assert lib.kvr_continue_batched(ctypes.byref(d), A, A, A, None, 2, A, A, 4, A, None, 0, None) == kvr.KVR_ERR_NULL
+    assert batched(lib, d, [0, 4], out=MIS) == kvr.KVR_ERR_ALIGN
+    assert batched(lib, d, [0, 4], kc=None) == kvr.KVR_ERR_NULL
+
+
+def test_python_binding_rejects_metadata_mismatch():
+    """The binding refuses tensors whose dtype or shape disagree with the descriptor."""
+    import torch
+    d = desc(n_q_heads=4, n_kv_heads=2, head_dim=64, capacity=8)
+    x = torch.zeros((2, 4, 64), dtype=torch.float32)
+    with pytest.raises(ValueError):
+        kvr._check(x, "Q", d, (2, 4, 64))       # CPU tensor and fp32 vs bf16
