@@ -23,7 +23,7 @@
  * Conventions shared by every entry point
  *   - Tensor pointers are DEVICE pointers owned by the caller; the library
  *     never allocates, frees or retains device memory and keeps no state
- *     beyond a per-device properties cache.
+ *     between calls (every call is thread-safe).
  *   - Layouts are dense row-major:
  *         Q, out            [tokens][n_q_heads][head_dim]
  *         K, V (new rows)   [tokens][n_kv_heads][head_dim]
@@ -136,7 +136,9 @@ int kvr_cache_append(const kvr_desc *desc, const void *Ks, const void *Vs, int64
  * Workspace bytes a continuation needs: n <= 1 for kvr_continue with
  * total_S = S, n >= 2 for kvr_continue_batched with total_S = cu[n].
  * A pure function of its arguments (no device query); returns 0 when no
- * workspace is needed and (size_t)-1 for an invalid descriptor.
+ * workspace is needed and (size_t)-1 for an invalid descriptor.  For a fixed
+ * S it never decreases with L_prefix: a workspace sized for the longest
+ * prefix serves every shorter one (e.g. all steps of a decode chain).
  */
 size_t kvr_workspace_bytes(const kvr_desc *desc, int64_t L_prefix, int64_t total_S, int32_t n);
 
