@@ -1,23 +1,25 @@
 // attn_bf16.hip -- causal grouped-query attention with a query offset, bf16
 // in, fp32 accumulate, for gfx950 (MI355X).  One kernel serves the three
 // modes of the library:
-//   prefill        keys are the new rows only, row tiles visited longest first;
+//   prefill        keys are the new rows only, row tiles visited longest first,
+//                  the new K/V rows are also written into the cache;
 //   continue       keys are the cached prefix plus the new rows, the prefix is
 //                  split across workgroups and merged afterwards (split-K);
 //   many readers   one shared prefix, one segment of rows per reader.
 //
 // Per workgroup: 4 waves x 32 query rows = 128 rows of one kv head; every
-// wave reads the same K/V tile from LDS (GQA sharing: the 4 query heads of a
+// wave reads the same K/V tile from LDS (GQA sharing: the query heads of a
 // group read each cached row once per workgroup).
 //
 // Per 64-key tile and wave, on MFMA v_mfma_f32_32x32x16_bf16:
 //   S^T[key][row] = K Q^T      (K rows from LDS, Q^T held in registers)
 //   online softmax on S^T: a lane owns one query row (column) and 16 keys of
-//   each 32-key sub-tile, so the row max / sum need only one cross-lane step
-//   O^T[d][row] += V^T P^T     (V^T from LDS, P^T straight from the S^T
-//                               accumulator registers, rounded to bf16)
+//   each 32-key sub-tile, so the row max / sum need one cross-lane step
+//   O^T[d][row] += V^T P^T     (V^T read from the row-major V tile with the
+//                               transposing LDS read, P^T straight from the
+//                               S^T accumulator registers, rounded to bf16)
 // Working on the transposed products keeps P in the registers the score
-// MFMA left it in: no LDS round trip for P.
+// MFMA left it in: no LDS round trip for P, no transposed copy of V.
 #include "kvr_internal.hpp"
 
 namespace kvr {
@@ -27,23 +29,31 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 
 constexpr int BN = kKeyTile;     // keys per tile
 constexpr int ROWS = kRowsBf16;  // rows per workgroup
 constexpr int THREADS = 256;
+// The running row maximum is only moved when a tile's maximum exceeds it by
+// more than this (log2 units): p = 2^(s - m) then stays below 2^8, which bf16
+// P and fp32 sums hold exactly as well as p <= 1, and the O rescale is skipped
+// for almost every tile.
+constexpr float kRescaleSlack = 8.f;
 
 template <int D>
 struct Tile {
     static constexpr int CH = D / 8;                  // 16-byte chunks per K/V row
-    static constexpr int KPT = BN * CH / THREADS;     // keys each thread stages (4 or 2)
-    static constexpr int K_PITCH = D * 2 + 16;        // LDS bytes per K row (pad: no bank conflicts)
-    static constexpr int V_PITCH = BN * 2 + 8;        // LDS bytes per V^T row (one head-dim index)
+    static constexpr int RPP = THREADS / CH;          // rows staged per pass
+    static constexpr int KPT = BN / RPP;              // passes (rows per thread): 4 or 2
+    static constexpr int K_PITCH = D * 2 + 16;        // LDS bytes per K row: conflict-free 16 B reads
+    static constexpr int V_PITCH = D * 2 + 64;        // LDS bytes per V row: conflict-free transposing reads
     static constexpr int K_BYTES = BN * K_PITCH;
-    static constexpr int V_BYTES = D * V_PITCH;
+    static constexpr int V_BYTES = BN * V_PITCH;
     static constexpr int STAGE = K_BYTES + V_BYTES;
     static constexpr int KSTEPS = D / 16;             // MFMA k-steps over the head dim
     static constexpr int DBLK = D / 32;               // 32-row blocks of O^T
-    static_assert(KPT * THREADS == BN * CH, "tile staging must cover the tile");
+    static_assert(KPT * RPP == BN, "tile staging must cover the tile");
 };
 
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
@@ -67,8 +77,14 @@ __device__ __forceinline__ int find_segment(const AttnParams &p, int tile) {
     return lo;
 }
 
-template <int D>
-__global__ __launch_bounds__(THREADS) void attn_bf16_kernel(const AttnParams p) {
+// MODE: kModePrefill  keys are the new rows only; row tiles longest first; the
+//                     workgroup that owns a token also writes its K/V row into
+//                     the cache (one launch does attention and the cache fill)
+//       kModeContinue cached prefix + new rows, prefix split across workgroups
+//       kModeReaders  cached prefix + each reader's own rows, no split
+template <int D, int MODE>
+__global__ __launch_bounds__(THREADS) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void attn_bf16_kernel(const AttnParams p) {
     using T = Tile<D>;
     __shared__ __attribute__((aligned(16))) unsigned char smem[2 * T::STAGE];
 
@@ -85,8 +101,8 @@ __global__ __launch_bounds__(THREADS) void attn_bf16_kernel(const AttnParams p) 
     b /= p.n_kv_heads;
     const int split = b % p.nsplit;
     b /= p.nsplit;
-    const int tile_lin = p.reverse ? (p.tiles_total - 1 - b) : b;
-    const int seg = find_segment(p, tile_lin);
+    const int tile_lin = MODE == kModePrefill ? (p.tiles_total - 1 - b) : b;
+    const int seg = MODE == kModeReaders ? find_segment(p, tile_lin) : 0;
     const int rt = tile_lin - p.seg_tile0[seg];
     const int tok0 = p.seg_tok0[seg];
     const int n_tok = p.seg_tok0[seg + 1] - tok0;
@@ -94,8 +110,7 @@ __global__ __launch_bounds__(THREADS) void attn_bf16_kernel(const AttnParams p) 
     const int R = G * n_tok;                       // rows of this segment for head g
     const int row0 = rt * ROWS;                    // first row of the workgroup
     const int row_last = min(row0 + ROWS, R) - 1;  // last valid row of the workgroup
-    const int64_t npre = p.n_prefix;
-    const int D_ = D;
+    const int64_t npre = MODE == kModePrefill ? 0 : p.n_prefix;
 
     // ---- this lane's query row
     const int r = row0 + wave * 32 + j;
@@ -107,7 +122,7 @@ __global__ __launch_bounds__(THREADS) void attn_bf16_kernel(const AttnParams p) 
     // ---- key range of this workgroup
     const int64_t k_all = npre + row_last / G + 1;   // keys any row of the workgroup may see
     int64_t kb = 0, ke = k_all;
-    if (p.nsplit > 1) {
+    if (MODE == kModeContinue && p.nsplit > 1) {
         kb = (int64_t)split * p.chunk;
         ke = (split == p.nsplit - 1) ? k_all : min(kb + p.chunk, npre);
     }
@@ -119,35 +134,45 @@ __global__ __launch_bounds__(THREADS) void attn_bf16_kernel(const AttnParams p) 
     // ---- Q^T fragments (MFMA B operand): column j, head-dim slots 16*ks + 8*grp + 0..7
     u32x4 qf[T::KSTEPS];
     {
-        const __bf16 *qrow = (const __bf16 *)p.q + ((int64_t)(tok0 + tok) * p.n_q_heads + head) * D_;
+        const __bf16 *qrow = (const __bf16 *)p.q + ((int64_t)(tok0 + tok) * p.n_q_heads + head) * D;
 #pragma unroll
-        for (int ks = 0; ks < T::KSTEPS; ++ks) {
+        for (int ks = 0; ks < T::KSTEPS; ++ks)
             qf[ks] = valid ? *(const u32x4 *)(qrow + 16 * ks + 8 * grp) : (u32x4){0, 0, 0, 0};
-        }
     }
 
-    // ---- staging map: thread -> (16-byte chunk c of the head dim, KPT consecutive keys)
+    // ---- staging map: thread -> 16-byte chunk sc of rows srow + RPP * i
     const int sc = tid % T::CH;
-    const int skq = tid / T::CH;
-    const __bf16 *kc = (const __bf16 *)p.kc + (int64_t)g * p.cap * D_ + 8 * sc;
-    const __bf16 *vc = (const __bf16 *)p.vc + (int64_t)g * p.cap * D_ + 8 * sc;
-    const int64_t nstride = (int64_t)p.n_kv_heads * D_;
-    const __bf16 *kn = (const __bf16 *)p.kn + (int64_t)tok0 * nstride + (int64_t)g * D_ + 8 * sc;
-    const __bf16 *vn = (const __bf16 *)p.vn + (int64_t)tok0 * nstride + (int64_t)g * D_ + 8 * sc;
+    const int srow = tid / T::CH;
+    const __bf16 *kc = (const __bf16 *)p.kc + (int64_t)g * p.cap * D + 8 * sc;
+    const __bf16 *vc = (const __bf16 *)p.vc + (int64_t)g * p.cap * D + 8 * sc;
+    const int64_t nstride = (int64_t)p.n_kv_heads * D;
+    const __bf16 *kn = (const __bf16 *)p.kn + (int64_t)tok0 * nstride + (int64_t)g * D + 8 * sc;
+    const __bf16 *vn = (const __bf16 *)p.vn + (int64_t)tok0 * nstride + (int64_t)g * D + 8 * sc;
+    __bf16 *kco = (__bf16 *)p.kc_out + (int64_t)g * p.cap * D + 8 * sc;   // prefill: cache rows out
+    __bf16 *vco = (__bf16 *)p.vc_out + (int64_t)g * p.cap * D + 8 * sc;
 
     u32x4 kreg[T::KPT], vreg[T::KPT];
+    // Rows past ke are clamped to a valid row: they lie beyond every row's
+    // causal bound, so they are masked out of every score and never count.
     auto gload = [&](int64_t k0) {
 #pragma unroll
         for (int i = 0; i < T::KPT; ++i) {
-            const int64_t key = k0 + skq * T::KPT + i;
-            if (key < ke) {
-                const __bf16 *ks_ = key < npre ? kc + key * D_ : kn + (key - npre) * nstride;
-                const __bf16 *vs_ = key < npre ? vc + key * D_ : vn + (key - npre) * nstride;
-                kreg[i] = *(const u32x4 *)ks_;
-                vreg[i] = *(const u32x4 *)vs_;
-            } else {
-                kreg[i] = (u32x4){0, 0, 0, 0};
-                vreg[i] = (u32x4){0, 0, 0, 0};
+            const int64_t key = k0 + srow + T::RPP * i;
+            const int64_t kk = key < ke ? key : ke - 1;
+            // branch-free choice of the source: cached row or new row
+            const bool in_cache = kk < npre;
+            const int64_t off = in_cache ? kk * D : (kk - npre) * nstride;
+            const __bf16 *kbase = in_cache ? kc : kn;
+            const __bf16 *vbase = in_cache ? vc : vn;
+            kreg[i] = *(const u32x4 *)(kbase + off);
+            vreg[i] = *(const u32x4 *)(vbase + off);
+            if constexpr (MODE == kModePrefill) {
+                // the workgroup holding the first query row of token `key` stores its cache row
+                const int64_t kr = key * G;
+                if (key < ke && kr >= row0 && kr < row0 + ROWS) {
+                    *(u32x4 *)(kco + key * D) = kreg[i];
+                    *(u32x4 *)(vco + key * D) = vreg[i];
+                }
             }
         }
     };
@@ -155,32 +180,19 @@ __global__ __launch_bounds__(THREADS) void attn_bf16_kernel(const AttnParams p) 
         unsigned char *ks_ = smem + stage * T::STAGE;
         unsigned char *vs_ = ks_ + T::K_BYTES;
 #pragma unroll
-        for (int i = 0; i < T::KPT; ++i)
-            *(u32x4 *)(ks_ + (skq * T::KPT + i) * T::K_PITCH + 16 * sc) = kreg[i];
-        // V^T: for each of the 8 head-dim indices of the chunk, KPT consecutive keys
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-            const int d = 8 * sc + e;
-            unsigned char *dst = vs_ + d * T::V_PITCH + skq * T::KPT * 2;
-            const int w = e >> 1;
-            if constexpr (T::KPT == 4) {
-                uint32_t a0 = vreg[0][w], a1 = vreg[1][w], a2 = vreg[2][w], a3 = vreg[3][w];
-                u32x2 o;
-                if (e & 1) {
-                    o[0] = (a0 >> 16) | (a1 & 0xffff0000u);
-                    o[1] = (a2 >> 16) | (a3 & 0xffff0000u);
-                } else {
-                    o[0] = (a0 & 0xffffu) | (a1 << 16);
-                    o[1] = (a2 & 0xffffu) | (a3 << 16);
-                }
-                *(u32x2 *)dst = o;
-            } else {
-                uint32_t a0 = vreg[0][w], a1 = vreg[1][w];
-                uint32_t o = (e & 1) ? ((a0 >> 16) | (a1 & 0xffff0000u)) : ((a0 & 0xffffu) | (a1 << 16));
-                *(uint32_t *)dst = o;
-            }
+        for (int i = 0; i < T::KPT; ++i) {
+            *(u32x4 *)(ks_ + (srow + T::RPP * i) * T::K_PITCH + 16 * sc) = kreg[i];
+            *(u32x4 *)(vs_ + (srow + T::RPP * i) * T::V_PITCH + 16 * sc) = vreg[i];
         }
     };
+
+    // Transposing V read: in each 16-lane group, lane i addresses
+    // V[key KB + i/4][d D0 + 4*(i%4) .. +3] and receives column d = D0 + i over
+    // the 4 keys KB..KB+3 -- the V^T MFMA operand slots of keys 4*grp + 0..3.
+    const int l16 = lane & 15;
+    const int g16 = lane >> 4;
+    const uint32_t v_lane = (4 * (g16 >> 1) + (l16 >> 2)) * T::V_PITCH + (16 * (g16 & 1) + 4 * (l16 & 3)) * 2;
+    const uint32_t k_lane = j * T::K_PITCH + 16 * grp;
 
     // ---- running softmax state of this lane's row (log2 domain, scaled)
     float m_run = -1e30f;
@@ -188,6 +200,7 @@ __global__ __launch_bounds__(THREADS) void attn_bf16_kernel(const AttnParams p) 
     f32x16 o_acc[T::DBLK];
 #pragma unroll
     for (int mt = 0; mt < T::DBLK; ++mt)
+#pragma unroll
         for (int i = 0; i < 16; ++i) o_acc[mt][i] = 0.f;
     const float c2 = p.scale_log2;
 
@@ -212,21 +225,24 @@ __global__ __launch_bounds__(THREADS) void attn_bf16_kernel(const AttnParams p) 
             f32x16 s[2];
 #pragma unroll
             for (int st = 0; st < 2; ++st) {
+#pragma unroll
                 for (int i = 0; i < 16; ++i) s[st][i] = 0.f;
 #pragma unroll
                 for (int ks = 0; ks < T::KSTEPS; ++ks) {
-                    u32x4 a = *(const u32x4 *)(ks_ + (32 * st + j) * T::K_PITCH + (16 * ks + 8 * grp) * 2);
+                    u32x4 a = *(const u32x4 *)(ks_ + k_lane + 32 * st * T::K_PITCH + 32 * ks);
                     s[st] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a), as_bf16x8(qf[ks]), s[st], 0, 0, 0);
                 }
             }
             // causal mask: key k0 + 32*st + 8*(i/4) + 4*grp + i%4 is visible iff <= pos
             if (k0 + BN > k_full) {
+                const int64_t lim64 = pos - k0;
+                const int lim = lim64 < -1 ? -1 : (lim64 > BN ? BN : (int)lim64);
 #pragma unroll
                 for (int st = 0; st < 2; ++st)
 #pragma unroll
                     for (int i = 0; i < 16; ++i) {
-                        const int64_t key = k0 + 32 * st + 8 * (i >> 2) + 4 * grp + (i & 3);
-                        if (key > pos) s[st][i] = -INFINITY;
+                        const int o = 32 * st + 8 * (i >> 2) + 4 * grp + (i & 3);
+                        if (o > lim) s[st][i] = -INFINITY;
                     }
             }
             float mx = -INFINITY;
@@ -234,11 +250,14 @@ __global__ __launch_bounds__(THREADS) void attn_bf16_kernel(const AttnParams p) 
             for (int st = 0; st < 2; ++st)
 #pragma unroll
                 for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s[st][i]);
-            mx = fmaxf(mx, __shfl_xor(mx, 32));
-            const float m_new = fmaxf(m_run, mx * c2);
-            const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-            m_run = m_new;
-            if (__ballot(alpha != 1.f)) {
+            mx = fmaxf(mx, __shfl_xor(mx, 32)) * c2;
+            // lazy rescale: move the reference only when p could exceed 2^kRescaleSlack
+            const bool need = mx > m_run + kRescaleSlack;
+            if (__ballot(need)) {
+                const float m_new = need ? mx : m_run;
+                const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+                m_run = m_new;
+                l_run *= alpha;
 #pragma unroll
                 for (int mt = 0; mt < T::DBLK; ++mt)
 #pragma unroll
@@ -250,26 +269,30 @@ __global__ __launch_bounds__(THREADS) void attn_bf16_kernel(const AttnParams p) 
             for (int st = 0; st < 2; ++st) {
 #pragma unroll
                 for (int i = 0; i < 16; i += 2) {
-                    const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[st][i], c2, -m_new));
-                    const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[st][i + 1], c2, -m_new));
-                    lsum += p0 + p1;
-                    pf[st][i >> 3][(i & 7) >> 1] = pack_bf16x2(p0, p1);
+                    const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[st][i], c2, -m_run));
+                    const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[st][i + 1], c2, -m_run));
+                    const uint32_t pk = pack_bf16x2(p0, p1);
+                    // normalise by the weights the PV product really uses (bf16-rounded):
+                    // the output is an exact convex combination of V rows
+                    lsum += __uint_as_float(pk << 16) + __uint_as_float(pk & 0xffff0000u);
+                    pf[st][i >> 3][(i & 7) >> 1] = pk;
                 }
             }
-            l_run = l_run * alpha + lsum;
+            l_run += lsum;
 
             // O^T += V^T P^T; P^T slot e of half kk is key 32*st + 16*kk + 8*(e/4) + 4*grp + e%4
 #pragma unroll
             for (int st = 0; st < 2; ++st)
 #pragma unroll
                 for (int kk = 0; kk < 2; ++kk) {
-                    const int kbase = 32 * st + 16 * kk + 4 * grp;
 #pragma unroll
                     for (int mt = 0; mt < T::DBLK; ++mt) {
-                        const unsigned char *vrow = vs_ + (32 * mt + j) * T::V_PITCH;
-                        u32x2 lo = *(const u32x2 *)(vrow + kbase * 2);
-                        u32x2 hi = *(const u32x2 *)(vrow + (kbase + 8) * 2);
-                        u32x4 a = {lo[0], lo[1], hi[0], hi[1]};
+                        const unsigned char *va = vs_ + v_lane + (32 * st + 16 * kk) * T::V_PITCH + 64 * mt;
+                        i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)va);
+                        i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)(va + 8 * T::V_PITCH));
+                        u32x2 lo2 = __builtin_bit_cast(u32x2, lo);
+                        u32x2 hi2 = __builtin_bit_cast(u32x2, hi);
+                        u32x4 a = {lo2[0], lo2[1], hi2[0], hi2[1]};
                         o_acc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a), as_bf16x8(pf[st][kk]),
                                                                            o_acc[mt], 0, 0, 0);
                     }
@@ -282,9 +305,9 @@ __global__ __launch_bounds__(THREADS) void attn_bf16_kernel(const AttnParams p) 
     // ---- epilogue
     const float l_tot = l_run + __shfl_xor(l_run, 32);
     if (!valid) return;
-    if (p.nsplit == 1) {
+    if (MODE != kModeContinue || p.nsplit == 1) {
         const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
-        __bf16 *orow = (__bf16 *)p.out + ((int64_t)(tok0 + tok) * p.n_q_heads + head) * D_;
+        __bf16 *orow = (__bf16 *)p.out + ((int64_t)(tok0 + tok) * p.n_q_heads + head) * D;
 #pragma unroll
         for (int mt = 0; mt < T::DBLK; ++mt)
 #pragma unroll
@@ -297,70 +320,106 @@ __global__ __launch_bounds__(THREADS) void attn_bf16_kernel(const AttnParams p) 
             }
     } else {
         const int64_t prow = ((int64_t)split * p.n_kv_heads + g) * p.rows_total + r;
-        float *po = p.ws + prow * D_;
+        float *po = p.ws + prow * D;
 #pragma unroll
         for (int mt = 0; mt < T::DBLK; ++mt)
 #pragma unroll
             for (int q4 = 0; q4 < 4; ++q4) {
                 const int d = 32 * mt + 8 * q4 + 4 * grp;
-                float4 v = make_float4(o_acc[mt][4 * q4], o_acc[mt][4 * q4 + 1], o_acc[mt][4 * q4 + 2],
-                                       o_acc[mt][4 * q4 + 3]);
-                *(float4 *)(po + d) = v;
+                *(float4 *)(po + d) = make_float4(o_acc[mt][4 * q4], o_acc[mt][4 * q4 + 1], o_acc[mt][4 * q4 + 2],
+                                                  o_acc[mt][4 * q4 + 3]);
             }
         if (grp == 0) {
-            float *pml = p.ws + (int64_t)p.nsplit * p.n_kv_heads * p.rows_total * D_ + prow * 2;
+            float *pml = p.ws + (int64_t)p.nsplit * p.n_kv_heads * p.rows_total * D + prow * 2;
             *(float2 *)pml = make_float2(m_run, l_tot);
         }
     }
 }
 
-// Combine the per-split partial results of every row (fixed split order, so
-// the result is reproducible bit for bit):
+// Combine the per-split partial results (fixed split order, so the result is
+// reproducible bit for bit):
 //   M = max_s m_s,  w_s = 2^(m_s - M),  out = sum_s w_s O_s / sum_s w_s l_s
+// Workgroup = 32 rows of one kv head x (D/4) lanes per row, each lane owning 4
+// consecutive head-dim values (16-byte loads, consecutive lanes consecutive
+// addresses).  The per-split weights of the 32 rows are computed once into LDS.
+constexpr int MERGE_ROWS = 32;
+
 template <int D>
-__global__ __launch_bounds__(256) void merge_bf16_kernel(const MergeParams p) {
-    constexpr int RPB = 256 / D;   // rows per block
-    const int r_in = threadIdx.x / D;
-    const int d = threadIdx.x % D;
-    const int64_t gr = (int64_t)blockIdx.x * RPB + r_in;   // over n_kv_heads * rows
-    if (gr >= (int64_t)p.n_kv_heads * p.rows) return;
-    const int g = (int)(gr / p.rows);
-    const int r = (int)(gr % p.rows);
+__global__ __launch_bounds__(MERGE_ROWS * D / 4) void merge_bf16_kernel(const MergeParams p) {
+    constexpr int LPR = D / 4;     // lanes per row
+    __shared__ float wts[kMaxSplits][MERGE_ROWS];
+    __shared__ float inv_l[MERGE_ROWS];
+    const int tid = threadIdx.x;
+    const int tiles_per_head = (p.rows + MERGE_ROWS - 1) / MERGE_ROWS;
+    const int g = blockIdx.x / tiles_per_head;
+    const int r0 = (blockIdx.x % tiles_per_head) * MERGE_ROWS;
     const int64_t per_split = (int64_t)p.n_kv_heads * p.rows;
     const float *ml = p.ws + (int64_t)p.nsplit * per_split * D;
-    float M = -INFINITY;
-    for (int s = 0; s < p.nsplit; ++s) M = fmaxf(M, ml[(s * per_split + gr) * 2]);
-    float acc = 0.f, l = 0.f;
-    for (int s = 0; s < p.nsplit; ++s) {
-        const float w = __builtin_amdgcn_exp2f(ml[(s * per_split + gr) * 2] - M);
-        l += w * ml[(s * per_split + gr) * 2 + 1];
-        acc += w * p.ws[(s * per_split + gr) * D + d];
+    const int64_t base_row = (int64_t)g * p.rows + r0;
+
+    if (tid < MERGE_ROWS && r0 + tid < p.rows) {
+        float M = -INFINITY;
+        for (int s = 0; s < p.nsplit; ++s) M = fmaxf(M, ml[(s * per_split + base_row + tid) * 2]);
+        float l = 0.f;
+        for (int s = 0; s < p.nsplit; ++s) {
+            const float2 v = *(const float2 *)(ml + (s * per_split + base_row + tid) * 2);
+            const float w = __builtin_amdgcn_exp2f(v.x - M);
+            wts[s][tid] = w;
+            l += w * v.y;
+        }
+        inv_l[tid] = l > 0.f ? 1.f / l : 0.f;
     }
+    __syncthreads();
+    const int rr = tid / LPR;
+    const int d4 = tid % LPR;
+    const int r = r0 + rr;
+    if (r >= p.rows) return;
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+    const float *src = p.ws + (base_row + rr) * D + 4 * d4;
+    for (int s = 0; s < p.nsplit; ++s) {
+        const float4 o = *(const float4 *)(src + s * per_split * D);
+        const float w = wts[s][rr];
+        acc.x += w * o.x; acc.y += w * o.y; acc.z += w * o.z; acc.w += w * o.w;
+    }
+    const float il = inv_l[rr];
     const int tok = r / p.group;
     const int head = g * p.group + r % p.group;
-    __bf16 *o = (__bf16 *)p.out + ((int64_t)tok * p.n_q_heads + head) * D + d;
-    *o = (__bf16)(l > 0.f ? acc / l : 0.f);
+    __bf16 *out = (__bf16 *)p.out + ((int64_t)tok * p.n_q_heads + head) * D + 4 * d4;
+    u32x2 v;
+    v[0] = pack_bf16x2(acc.x * il, acc.y * il);
+    v[1] = pack_bf16x2(acc.z * il, acc.w * il);
+    *(u32x2 *)out = v;
+}
+
+template <int D>
+hipError_t launch_d(const AttnParams &p, int mode, int grid, hipStream_t s) {
+    switch (mode) {
+        case kModePrefill:
+            hipLaunchKernelGGL((attn_bf16_kernel<D, kModePrefill>), dim3(grid), dim3(THREADS), 0, s, p);
+            break;
+        case kModeContinue:
+            hipLaunchKernelGGL((attn_bf16_kernel<D, kModeContinue>), dim3(grid), dim3(THREADS), 0, s, p);
+            break;
+        default:
+            hipLaunchKernelGGL((attn_bf16_kernel<D, kModeReaders>), dim3(grid), dim3(THREADS), 0, s, p);
+            break;
+    }
+    return hipGetLastError();
 }
 
 }  // namespace
 
-hipError_t launch_attn_bf16(const AttnParams &p, int head_dim, int grid, hipStream_t s) {
-    if (head_dim == 128)
-        hipLaunchKernelGGL(attn_bf16_kernel<128>, dim3(grid), dim3(THREADS), 0, s, p);
-    else
-        hipLaunchKernelGGL(attn_bf16_kernel<64>, dim3(grid), dim3(THREADS), 0, s, p);
-    return hipGetLastError();
+hipError_t launch_attn_bf16(const AttnParams &p, int head_dim, int mode, int grid, hipStream_t s) {
+    return head_dim == 128 ? launch_d<128>(p, mode, grid, s) : launch_d<64>(p, mode, grid, s);
 }
 
 hipError_t launch_merge_bf16(const MergeParams &p, int head_dim, hipStream_t s) {
-    const int64_t rows = (int64_t)p.n_kv_heads * p.rows;
-    if (head_dim == 128) {
-        const int grid = (int)((rows + 1) / 2);
-        hipLaunchKernelGGL(merge_bf16_kernel<128>, dim3(grid), dim3(256), 0, s, p);
-    } else {
-        const int grid = (int)((rows + 3) / 4);
-        hipLaunchKernelGGL(merge_bf16_kernel<64>, dim3(grid), dim3(256), 0, s, p);
-    }
+    const int tiles = (p.rows + MERGE_ROWS - 1) / MERGE_ROWS;
+    const int grid = tiles * p.n_kv_heads;
+    if (head_dim == 128)
+        hipLaunchKernelGGL(merge_bf16_kernel<128>, dim3(grid), dim3(MERGE_ROWS * 128 / 4), 0, s, p);
+    else
+        hipLaunchKernelGGL(merge_bf16_kernel<64>, dim3(grid), dim3(MERGE_ROWS * 64 / 4), 0, s, p);
     return hipGetLastError();
 }
 

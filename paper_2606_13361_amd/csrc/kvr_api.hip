@@ -57,6 +57,7 @@ Split plan_split(const kvr_desc *d, int64_t L_prefix, int64_t S) {
     int64_t want = (kTargetWorkgroups + base - 1) / base;
     const int64_t most = (L_prefix + kMinSplitKeys - 1) / kMinSplitKeys;
     if (want > most) want = most;
+    if (want > kMaxSplits) want = kMaxSplits;
     if (want <= 1) return s;
     int64_t chunk = (L_prefix + want - 1) / want;
     chunk = (chunk + kKeyTile - 1) / kKeyTile * kKeyTile;
@@ -64,7 +65,9 @@ Split plan_split(const kvr_desc *d, int64_t L_prefix, int64_t S) {
     if (n <= 1) return s;
     s.nsplit = (int32_t)n;
     s.chunk = chunk;
-    s.ws_bytes = (size_t)n * d->n_kv_heads * rows * (d->head_dim + 2) * sizeof(float);
+    // sized by the requested split count (n <= want): non-decreasing in
+    // L_prefix, so one workspace serves every shorter prefix of a decode chain
+    s.ws_bytes = (size_t)want * d->n_kv_heads * rows * (d->head_dim + 2) * sizeof(float);
     return s;
 }
 
@@ -82,12 +85,32 @@ void fill_common(AttnParams &p, const kvr_desc *d) {
 }
 
 // One segment: rows of tokens [0, n_tok).
-int launch_single(const kvr_desc *d, const void *Q, const void *K, const void *V, const void *kc,
-                  const void *vc, int64_t n_prefix, int64_t n_tok, void *out, const Split &sp, void *ws,
-                  bool reverse, hipStream_t stream) {
+int append_impl(const kvr_desc *d, const void *Ks, const void *Vs, int64_t S, void *kc, void *vc,
+                int64_t L_cur, hipStream_t stream) {
+    AppendParams a;
+    a.k = Ks; a.v = Vs; a.kc = kc; a.vc = vc;
+    a.S = S; a.L_cur = L_cur; a.cap = d->capacity;
+    a.n_kv_heads = d->n_kv_heads;
+    a.row_chunks = d->head_dim * elt_bytes(d) / 16;
+    return to_status(launch_append(a, stream));
+}
+
+// mode kModePrefill: kc/vc are the caches to fill (bf16: in the attention
+// kernel itself); kModeContinue: kc/vc are the cached prefix (read only).
+int launch_single(const kvr_desc *d, int mode, const void *Q, const void *K, const void *V, void *kc,
+                  void *vc, int64_t n_prefix, int64_t n_tok, void *out, const Split &sp, void *ws,
+                  hipStream_t stream) {
     AttnParams p;
     fill_common(p, d);
-    p.q = Q; p.kn = K; p.vn = V; p.kc = kc; p.vc = vc; p.out = out;
+    p.q = Q; p.kn = K; p.vn = V; p.out = out;
+    const bool reverse = mode == kModePrefill;
+    if (mode == kModePrefill) {
+        p.kc_out = kc;
+        p.vc_out = vc;
+    } else {
+        p.kc = kc;
+        p.vc = vc;
+    }
     p.ws = (float *)ws;
     p.n_prefix = n_prefix;
     p.nsplit = sp.nsplit;
@@ -108,8 +131,16 @@ int launch_single(const kvr_desc *d, const void *Q, const void *K, const void *V
     const int64_t grid = tiles * p.nsplit * p.n_kv_heads;
     if (grid <= 0) return KVR_OK;
     if (grid > 0x7fffffff) return KVR_ERR_SHAPE;
-    hipError_t e = d->dtype == KVR_BF16 ? launch_attn_bf16(p, d->head_dim, (int)grid, stream)
-                                        : launch_attn_f32(p, d->head_dim, (int)grid, stream);
+    hipError_t e;
+    if (d->dtype == KVR_BF16) {
+        e = launch_attn_bf16(p, d->head_dim, mode, (int)grid, stream);
+    } else {
+        if (mode == kModePrefill) {   // the fp32 kernel does not write the cache itself
+            const int st = append_impl(d, K, V, n_tok, kc, vc, 0, stream);
+            if (st) return st;
+        }
+        e = launch_attn_f32(p, d->head_dim, (int)grid, stream);
+    }
     if (e != hipSuccess) return KVR_ERR_DEVICE;
     if (p.nsplit > 1) {
         MergeParams m;
@@ -121,15 +152,6 @@ int launch_single(const kvr_desc *d, const void *Q, const void *K, const void *V
     return KVR_OK;
 }
 
-int append_impl(const kvr_desc *d, const void *Ks, const void *Vs, int64_t S, void *kc, void *vc,
-                int64_t L_cur, hipStream_t stream) {
-    AppendParams a;
-    a.k = Ks; a.v = Vs; a.kc = kc; a.vc = vc;
-    a.S = S; a.L_cur = L_cur; a.cap = d->capacity;
-    a.n_kv_heads = d->n_kv_heads;
-    a.row_chunks = d->head_dim * elt_bytes(d) / 16;
-    return to_status(launch_append(a, stream));
-}
 
 }  // namespace
 }  // namespace kvr
@@ -171,11 +193,9 @@ int kvr_prefill(const kvr_desc *desc, const void *Q, const void *K, const void *
     if (!aligned16(Q) || !aligned16(K) || !aligned16(V) || !aligned16(out) || !aligned16(kcache) ||
         !aligned16(vcache))
         return KVR_ERR_ALIGN;
-    hipStream_t s = (hipStream_t)stream;
-    st = append_impl(desc, K, V, L, kcache, vcache, 0, s);
-    if (st) return st;
     Split none{1, 0, 0};
-    return launch_single(desc, Q, K, V, nullptr, nullptr, 0, L, out, none, nullptr, true, s);
+    return launch_single(desc, kModePrefill, Q, K, V, kcache, vcache, 0, L, out, none, nullptr,
+                         (hipStream_t)stream);
 }
 
 int kvr_continue(const kvr_desc *desc, const void *Qs, const void *Ks, const void *Vs, const void *kcache,
@@ -194,8 +214,8 @@ int kvr_continue(const kvr_desc *desc, const void *Qs, const void *Ks, const voi
     if (!aligned16(Qs) || !aligned16(Ks) || !aligned16(Vs) || !aligned16(out) || !aligned16(kcache) ||
         !aligned16(vcache) || !aligned16(ws))
         return KVR_ERR_ALIGN;
-    return launch_single(desc, Qs, Ks, Vs, kcache, vcache, L_prefix, S, out, sp, ws, false,
-                         (hipStream_t)stream);
+    return launch_single(desc, kModeContinue, Qs, Ks, Vs, (void *)kcache, (void *)vcache, L_prefix, S, out,
+                         sp, ws, (hipStream_t)stream);
 }
 
 int kvr_continue_batched(const kvr_desc *desc, const void *Qs, const void *Ks, const void *Vs,
@@ -247,7 +267,8 @@ int kvr_continue_batched(const kvr_desc *desc, const void *Qs, const void *Ks, c
         p.tiles_total = tiles;
         p.rows_total = 0;
         const int64_t grid = (int64_t)tiles * p.n_kv_heads;
-        hipError_t e = desc->dtype == KVR_BF16 ? launch_attn_bf16(p, desc->head_dim, (int)grid, (hipStream_t)stream)
+        hipError_t e = desc->dtype == KVR_BF16 ? launch_attn_bf16(p, desc->head_dim, kModeReaders, (int)grid,
+                                                                  (hipStream_t)stream)
                                                : launch_attn_f32(p, desc->head_dim, (int)grid, (hipStream_t)stream);
         if (e != hipSuccess) return KVR_ERR_DEVICE;
     }

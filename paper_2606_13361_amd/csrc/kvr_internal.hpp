@@ -21,6 +21,8 @@ struct AttnParams {
     const void *kc;  // cached keys   [n_kv_heads][cap][D]
     const void *vc;  // cached values [n_kv_heads][cap][D]
     void *out;       // [tokens][n_q_heads][D]
+    void *kc_out;    // prefill: cache the new K rows go to [n_kv_heads][cap][D]
+    void *vc_out;
     float *ws;       // split partials: O [nsplit][Hkv][rows][D], then (m, l) [nsplit][Hkv][rows][2]
     int64_t cap;
     int64_t n_prefix;  // cached keys, positions [0, n_prefix); every query row sees them all
@@ -30,7 +32,7 @@ struct AttnParams {
     float scale;        // softmax scale
     float scale_log2;   // scale * log2(e)
     int32_t n_seg;      // segments (independent readers); 1 for prefill / continue
-    int32_t reverse;    // visit row tiles last-first (longest causal rows first)
+    int32_t reverse;    // fp32 path: visit row tiles last-first (longest causal rows first)
     int32_t tiles_total;
     int32_t rows_total;  // rows per kv head (partials indexing, single segment)
     int32_t seg_tok0[kMaxSegments + 1];   // packed token offset of each segment (cu_seqlens)
@@ -53,8 +55,10 @@ struct MergeParams {
     int32_t nsplit, n_q_heads, n_kv_heads, group, rows;
 };
 
+enum { kModePrefill = 0, kModeContinue = 1, kModeReaders = 2 };
+
 // bf16 path (MFMA), D in {64, 128}
-hipError_t launch_attn_bf16(const AttnParams &p, int head_dim, int grid, hipStream_t s);
+hipError_t launch_attn_bf16(const AttnParams &p, int head_dim, int mode, int grid, hipStream_t s);
 hipError_t launch_merge_bf16(const MergeParams &p, int head_dim, hipStream_t s);
 // fp32 path (VALU), D in {64, 128}
 hipError_t launch_attn_f32(const AttnParams &p, int head_dim, int grid, hipStream_t s);
@@ -65,5 +69,6 @@ hipError_t launch_append(const AppendParams &p, hipStream_t s);
 constexpr int kRowsBf16 = 128;  // query rows per workgroup, bf16 path
 constexpr int kRowsF32 = 64;    // query rows per workgroup, fp32 path
 constexpr int kKeyTile = 64;    // keys per tile (split chunks are multiples of it)
+constexpr int kMaxSplits = 256; // key splits of one continuation (merge kernel LDS table)
 
 }  // namespace kvr

@@ -164,6 +164,10 @@ def test_workspace_bytes_is_a_pure_plan(lib):
     assert f(32768, 1) % (8 * 4 * (128 + 2) * 4) == 0   # whole partial rows of fp32
     assert f(32768, 24, 1, desc(dtype=kvr.KVR_F32, capacity=1 << 16)) == 0
     assert f(-1, 3) == ctypes.c_size_t(-1).value
+    # never decreases with the prefix length (one buffer for a whole decode chain)
+    for S in (1, 24, 100):
+        sizes = [f(L, S) for L in range(0, 40000, 97)]
+        assert all(a <= b for a, b in zip(sizes, sizes[1:])), S
 
 
 def test_append_errors(lib):

@@ -170,7 +170,12 @@ def test_stress_softmax(kind):
     # allowance on top (and one bf16 ulp, |x| * 2^-7, between two GPU results).
     excess(full[rows], want, TOL[torch.bfloat16], 2.0 ** -8)
     excess(cont, want[-S:], TOL[torch.bfloat16], 2.0 ** -8)
-    excess(cont, full[Lp:].double().cpu().numpy(), CLAIM1_TOL, 2.0 ** -7)
+    # Between two GPU results also: the running maximum is moved lazily, so the
+    # largest softmax weight 2^d (0 < d <= 8) is itself rounded to bf16; with
+    # w its normalised weight that moves the output by at most
+    # 2^-9 * w (1 - w) * (max v - min v) <= 2^-11 * (max v - min v) in each result.
+    spread = float(v.float().max() - v.float().min())
+    excess(cont, full[Lp:].double().cpu().numpy(), CLAIM1_TOL + 2.0 ** -10 * spread, 2.0 ** -7)
 
 
 def excess(gpu, want, tol, rel):
