@@ -43,6 +43,10 @@ def parse():
     ap.add_argument("--no-decode36", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="target CPU-oracle sample time")
+    ap.add_argument("--sweep-lengths", type=str, default=None,
+                    help="comma-separated prefix lengths for the sweep (default: all four)")
+    ap.add_argument("--sweep-only", action="store_true",
+                    help="skip the layer step (for profiling one sweep length)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="first run one plain 1 GiB device copy (reference for HBM byte counters)")
     return ap.parse_args()
@@ -119,6 +123,13 @@ def main():
         rec(5)
         kvr.kvr_cache_append(desc, dk, dv, 1, kc, vc, n)
         rec(6)
+
+    if args.sweep_only:
+        res = {"sweep": sweep(torch, kvr, A, W, dev, stream,
+                              [int(x) for x in args.sweep_lengths.split(",")] if args.sweep_lengths
+                              else list(W.SWEEP_L))}
+        print(json.dumps(res), flush=True)
+        return
 
     for _ in range(args.warmup):
         step()
@@ -201,7 +212,8 @@ def main():
     }
 
     if not args.no_sweep:
-        result["sweep"] = sweep(torch, kvr, A, W, dev, stream)
+        lens_ = [int(x) for x in args.sweep_lengths.split(",")] if args.sweep_lengths else list(W.SWEEP_L)
+        result["sweep"] = sweep(torch, kvr, A, W, dev, stream, lens_)
     if not args.no_decode36:
         result["decode36"] = decode36(torch, kvr, A, W, dev, stream)
     if not args.no_cpu_baseline:
@@ -219,13 +231,13 @@ def timed(torch, stream, fn, iters):
     return [ev[i].elapsed_time(ev[i + 1]) * 1e-3 for i in range(iters)]
 
 
-def sweep(torch, kvr, A, W, dev, stream):
+def sweep(torch, kvr, A, W, dev, stream, lengths):
     """Prefill of L+24 vs continuation of 24 over L, L in {1024, 4096, 16384, 32768}."""
     sh = W.QWEN
     Hq, Hkv, D = sh.n_q_heads, sh.n_kv_heads, sh.head_dim
     S = W.SWEEP_S
     rows = []
-    for L in W.SWEEP_L:
+    for L in lengths:
         n = L + S
         q, k, v = W.qkv_device(n, sh, seed=L, device=dev)
         desc = kvr.make_desc(Hq, Hkv, D, torch.bfloat16, n)

@@ -67,6 +67,22 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
 
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
 
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+__device__ const bf16x2 kOnes = {(__bf16)1.0f, (__bf16)1.0f};
+
+// Lanes l and l^32 hold the two halves of one query row.  v_permlane32_swap
+// exchanges the upper half of its first operand with the lower half of its
+// second; with both operands x the two results are {x[l], x[l^32]} in some
+// order, so their max / sum is the row's (and the same bits in both lanes).
+__device__ __forceinline__ float pair_max(float x) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float pair_sum(float x) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
 // Locate the segment (reader) that owns a linear row-tile index.
 __device__ __forceinline__ int find_segment(const AttnParams &p, int tile) {
     int lo = 0, hi = p.n_seg - 1;
@@ -152,26 +168,59 @@ void attn_bf16_kernel(const AttnParams p) {
     __bf16 *vco = (__bf16 *)p.vc_out + (int64_t)g * p.cap * D + 8 * sc;
 
     u32x4 kreg[T::KPT], vreg[T::KPT];
-    // Rows past ke are clamped to a valid row: they lie beyond every row's
-    // causal bound, so they are masked out of every score and never count.
+    // Interior tiles (all 64 rows from one source, none past ke, no cache row
+    // to store) load with one uniform base address per tile and fixed
+    // per-thread byte offsets.  Only the tiles at the prefix/new boundary, at
+    // the end of the range or holding this workgroup's own prefill tokens take
+    // the general path, where rows past ke are clamped to a valid row (they lie
+    // beyond every row's causal bound, so they are masked and never count).
+    const uint32_t cache_off = (uint32_t)(srow * D * 2 + 16 * sc);
+    const uint32_t new_off = (uint32_t)(srow * nstride * 2 + 16 * sc);
+    const uint32_t cache_pass = (uint32_t)(T::RPP * D * 2);
+    const uint32_t new_pass = (uint32_t)(T::RPP * nstride * 2);
+    const int64_t cache_end = ke < npre ? ke : npre;   // keys [.., cache_end) come from the cache
+    int64_t own_lo = 0, own_hi = -1;                   // prefill tokens whose cache row this WG stores
+    if constexpr (MODE == kModePrefill) {
+        own_lo = (row0 + G - 1) / G;
+        own_hi = (row0 + ROWS - 1) / G;
+    }
+    const unsigned char *kc0 = (const unsigned char *)p.kc + (int64_t)g * p.cap * D * 2;
+    const unsigned char *vc0 = (const unsigned char *)p.vc + (int64_t)g * p.cap * D * 2;
+    const unsigned char *kn0 = (const unsigned char *)p.kn + ((int64_t)tok0 * nstride + (int64_t)g * D) * 2;
+    const unsigned char *vn0 = (const unsigned char *)p.vn + ((int64_t)tok0 * nstride + (int64_t)g * D) * 2;
     auto gload = [&](int64_t k0) {
+        const bool own = MODE == kModePrefill && k0 <= own_hi && k0 + BN > own_lo;
+        if (k0 + BN <= cache_end) {
+            const unsigned char *kb_ = kc0 + k0 * D * 2, *vb_ = vc0 + k0 * D * 2;
 #pragma unroll
-        for (int i = 0; i < T::KPT; ++i) {
-            const int64_t key = k0 + srow + T::RPP * i;
-            const int64_t kk = key < ke ? key : ke - 1;
-            // branch-free choice of the source: cached row or new row
-            const bool in_cache = kk < npre;
-            const int64_t off = in_cache ? kk * D : (kk - npre) * nstride;
-            const __bf16 *kbase = in_cache ? kc : kn;
-            const __bf16 *vbase = in_cache ? vc : vn;
-            kreg[i] = *(const u32x4 *)(kbase + off);
-            vreg[i] = *(const u32x4 *)(vbase + off);
-            if constexpr (MODE == kModePrefill) {
-                // the workgroup holding the first query row of token `key` stores its cache row
-                const int64_t kr = key * G;
-                if (key < ke && kr >= row0 && kr < row0 + ROWS) {
-                    *(u32x4 *)(kco + key * D) = kreg[i];
-                    *(u32x4 *)(vco + key * D) = vreg[i];
+            for (int i = 0; i < T::KPT; ++i) {
+                kreg[i] = *(const u32x4 *)(kb_ + cache_off + i * cache_pass);
+                vreg[i] = *(const u32x4 *)(vb_ + cache_off + i * cache_pass);
+            }
+        } else if (k0 >= npre && k0 + BN <= ke && !own) {
+            const unsigned char *kb_ = kn0 + (k0 - npre) * nstride * 2, *vb_ = vn0 + (k0 - npre) * nstride * 2;
+#pragma unroll
+            for (int i = 0; i < T::KPT; ++i) {
+                kreg[i] = *(const u32x4 *)(kb_ + new_off + i * new_pass);
+                vreg[i] = *(const u32x4 *)(vb_ + new_off + i * new_pass);
+            }
+        } else {
+#pragma unroll
+            for (int i = 0; i < T::KPT; ++i) {
+                const int64_t key = k0 + srow + T::RPP * i;
+                const int64_t kk = key < ke ? key : ke - 1;
+                const bool in_cache = kk < npre;
+                const int64_t off = in_cache ? kk * D : (kk - npre) * nstride;
+                const __bf16 *kbase = in_cache ? kc : kn;
+                const __bf16 *vbase = in_cache ? vc : vn;
+                kreg[i] = *(const u32x4 *)(kbase + off);
+                vreg[i] = *(const u32x4 *)(vbase + off);
+                if constexpr (MODE == kModePrefill) {
+                    // the workgroup holding the first query row of token `key` stores its cache row
+                    if (key >= own_lo && key <= own_hi && key < ke) {
+                        *(u32x4 *)(kco + key * D) = kreg[i];
+                        *(u32x4 *)(vco + key * D) = vreg[i];
+                    }
                 }
             }
         }
@@ -250,7 +299,7 @@ void attn_bf16_kernel(const AttnParams p) {
             for (int st = 0; st < 2; ++st)
 #pragma unroll
                 for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s[st][i]);
-            mx = fmaxf(mx, __shfl_xor(mx, 32)) * c2;
+            mx = pair_max(mx) * c2;
             // lazy rescale: move the reference only when p could exceed 2^kRescaleSlack
             const bool need = mx > m_run + kRescaleSlack;
             if (__ballot(need)) {
@@ -274,7 +323,7 @@ void attn_bf16_kernel(const AttnParams p) {
                     const uint32_t pk = pack_bf16x2(p0, p1);
                     // normalise by the weights the PV product really uses (bf16-rounded):
                     // the output is an exact convex combination of V rows
-                    lsum += __uint_as_float(pk << 16) + __uint_as_float(pk & 0xffff0000u);
+                    lsum = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, pk), kOnes, lsum, false);
                     pf[st][i >> 3][(i & 7) >> 1] = pk;
                 }
             }
@@ -303,7 +352,7 @@ void attn_bf16_kernel(const AttnParams p) {
     }
 
     // ---- epilogue
-    const float l_tot = l_run + __shfl_xor(l_run, 32);
+    const float l_tot = pair_sum(l_run);
     if (!valid) return;
     if (MODE != kModeContinue || p.nsplit == 1) {
         const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
