@@ -1,103 +1,41 @@
 // attn_bf16.hip -- causal grouped-query attention with a query offset, bf16
-// in, fp32 accumulate, for gfx950 (MI355X).  One kernel serves the three
-// modes of the library:
-//   prefill        keys are the new rows only, row tiles visited longest first,
-//                  the new K/V rows are also written into the cache;
-//   continue       keys are the cached prefix plus the new rows, the prefix is
-//                  split across workgroups and merged afterwards (split-K);
-//   many readers   one shared prefix, one segment of rows per reader.
+// in, fp32 accumulate, for gfx950 (MI355X): the register-staged member of the
+// kernel family.  It serves prefill (all head dims) and every mode at head_dim
+// 64; continue and many-readers at head_dim 128 use the streamed kernel in
+// attn_stream.hip.  The per-tile arithmetic is shared (attn_common.hpp).
+//
+//   prefill   keys are the new rows only, row tiles visited longest first, and
+//             the workgroup owning a token also writes its K/V row into the
+//             cache from the registers it staged (one launch does both)
+//   continue  cached prefix + new rows, prefix split across workgroups
+//   readers   shared prefix + each reader's own rows
 //
 // Per workgroup: 4 waves x 32 query rows = 128 rows of one kv head; every
-// wave reads the same K/V tile from LDS (GQA sharing: the query heads of a
-// group read each cached row once per workgroup).
-//
-// Per 64-key tile and wave, on MFMA v_mfma_f32_32x32x16_bf16:
-//   S^T[key][row] = K Q^T      (K rows from LDS, Q^T held in registers)
-//   online softmax on S^T: a lane owns one query row (column) and 16 keys of
-//   each 32-key sub-tile, so the row max / sum need one cross-lane step
-//   O^T[d][row] += V^T P^T     (V^T read from the row-major V tile with the
-//                               transposing LDS read, P^T straight from the
-//                               S^T accumulator registers, rounded to bf16)
-// Working on the transposed products keeps P in the registers the score
-// MFMA left it in: no LDS round trip for P, no transposed copy of V.
-#include "kvr_internal.hpp"
+// wave reads the same K/V tile from LDS (GQA sharing).  Tiles of 64 keys are
+// staged global -> registers -> LDS, double buffered: the next tile's global
+// loads are issued before the current tile's math.  K rows are padded to a
+// 16-byte multiple + 16 (conflict-free 16-byte reads), V rows by 64 bytes
+// (conflict-free transposing reads).
+#include "attn_common.hpp"
 
 namespace kvr {
 namespace {
 
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef float f32x16 __attribute__((ext_vector_type(16)));
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
-typedef short i16x4 __attribute__((ext_vector_type(4)));
-typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
-
-constexpr int BN = kKeyTile;     // keys per tile
-constexpr int ROWS = kRowsBf16;  // rows per workgroup
-constexpr int THREADS = 256;
-// The running row maximum is only moved when a tile's maximum exceeds it by
-// more than this (log2 units): p = 2^(s - m) then stays below 2^8, which bf16
-// P and fp32 sums hold exactly as well as p <= 1, and the O rescale is skipped
-// for almost every tile.
-constexpr float kRescaleSlack = 8.f;
+using namespace dev;
 
 template <int D>
 struct Tile {
     static constexpr int CH = D / 8;                  // 16-byte chunks per K/V row
     static constexpr int RPP = THREADS / CH;          // rows staged per pass
     static constexpr int KPT = BN / RPP;              // passes (rows per thread): 4 or 2
-    static constexpr int K_PITCH = D * 2 + 16;        // LDS bytes per K row: conflict-free 16 B reads
-    static constexpr int V_PITCH = D * 2 + 64;        // LDS bytes per V row: conflict-free transposing reads
+    static constexpr int K_PITCH = D * 2 + 16;        // LDS bytes per K row
+    static constexpr int V_PITCH = D * 2 + 64;        // LDS bytes per V row
     static constexpr int K_BYTES = BN * K_PITCH;
     static constexpr int V_BYTES = BN * V_PITCH;
     static constexpr int STAGE = K_BYTES + V_BYTES;
-    static constexpr int KSTEPS = D / 16;             // MFMA k-steps over the head dim
-    static constexpr int DBLK = D / 32;               // 32-row blocks of O^T
     static_assert(KPT * RPP == BN, "tile staging must cover the tile");
 };
 
-__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-    // v_cvt_pk_bf16_f32: round to nearest even
-    typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-    bf16x2 v;
-    v[0] = (__bf16)lo;
-    v[1] = (__bf16)hi;
-    return __builtin_bit_cast(uint32_t, v);
-}
-
-__device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
-
-typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-__device__ const bf16x2 kOnes = {(__bf16)1.0f, (__bf16)1.0f};
-
-// Lanes l and l^32 hold the two halves of one query row.  v_permlane32_swap
-// exchanges the upper half of its first operand with the lower half of its
-// second; with both operands x the two results are {x[l], x[l^32]} in some
-// order, so their max / sum is the row's (and the same bits in both lanes).
-__device__ __forceinline__ float pair_max(float x) {
-    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
-}
-__device__ __forceinline__ float pair_sum(float x) {
-    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
-}
-
-// Locate the segment (reader) that owns a linear row-tile index.
-__device__ __forceinline__ int find_segment(const AttnParams &p, int tile) {
-    int lo = 0, hi = p.n_seg - 1;
-    while (lo < hi) {
-        int mid = (lo + hi + 1) >> 1;
-        if (p.seg_tile0[mid] <= tile) lo = mid; else hi = mid - 1;
-    }
-    return lo;
-}
-
-// MODE: kModePrefill  keys are the new rows only; row tiles longest first; the
-//                     workgroup that owns a token also writes its K/V row into
-//                     the cache (one launch does attention and the cache fill)
-//       kModeContinue cached prefix + new rows, prefix split across workgroups
-//       kModeReaders  cached prefix + each reader's own rows, no split
 template <int D, int MODE>
 __global__ __launch_bounds__(THREADS) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void attn_bf16_kernel(const AttnParams p) {
@@ -110,49 +48,30 @@ void attn_bf16_kernel(const AttnParams p) {
     const int j = lane & 31;      // query row (MFMA column) owned by this lane
     const int grp = lane >> 5;    // which half of each key quad-set this lane holds
 
-    // ---- which work item: kv head fastest (consecutive workgroups land on
-    // different XCDs, so each XCD keeps one head's K/V in its L2)
-    int b = blockIdx.x;
-    const int g = b % p.n_kv_heads;
-    b /= p.n_kv_heads;
-    const int split = b % p.nsplit;
-    b /= p.nsplit;
-    const int tile_lin = MODE == kModePrefill ? (p.tiles_total - 1 - b) : b;
-    const int seg = MODE == kModeReaders ? find_segment(p, tile_lin) : 0;
-    const int rt = tile_lin - p.seg_tile0[seg];
-    const int tok0 = p.seg_tok0[seg];
-    const int n_tok = p.seg_tok0[seg + 1] - tok0;
-    const int G = p.group;
-    const int R = G * n_tok;                       // rows of this segment for head g
-    const int row0 = rt * ROWS;                    // first row of the workgroup
-    const int row_last = min(row0 + ROWS, R) - 1;  // last valid row of the workgroup
-    const int64_t npre = MODE == kModePrefill ? 0 : p.n_prefix;
+    const Work w = decode_work<MODE>(p);
+    const int G = w.G;
+    const int row0 = w.row0;
+    const int64_t npre = w.npre, kb = w.kb, ke = w.ke;
+    const int g = w.g;
+    const int tok0 = w.tok0;
 
     // ---- this lane's query row
     const int r = row0 + wave * 32 + j;
-    const bool valid = r < R;
+    const bool valid = r < w.R;
     const int tok = valid ? r / G : 0;
     const int head = g * G + (valid ? r % G : 0);
     const int64_t pos = valid ? npre + tok : -1;   // absolute position; -1 sees nothing
-
-    // ---- key range of this workgroup
-    const int64_t k_all = npre + row_last / G + 1;   // keys any row of the workgroup may see
-    int64_t kb = 0, ke = k_all;
-    if (MODE == kModeContinue && p.nsplit > 1) {
-        kb = (int64_t)split * p.chunk;
-        ke = (split == p.nsplit - 1) ? k_all : min(kb + p.chunk, npre);
-    }
     // rows of this wave see every key below k_full (no mask needed there)
     const int wrow0 = row0 + wave * 32;
-    const bool wave_active = wrow0 < R;
+    const bool wave_active = wrow0 < w.R;
     const int64_t k_full = wave_active ? npre + wrow0 / G + 1 : 0;
 
     // ---- Q^T fragments (MFMA B operand): column j, head-dim slots 16*ks + 8*grp + 0..7
-    u32x4 qf[T::KSTEPS];
+    u32x4 qf[D / 16];
     {
         const __bf16 *qrow = (const __bf16 *)p.q + ((int64_t)(tok0 + tok) * p.n_q_heads + head) * D;
 #pragma unroll
-        for (int ks = 0; ks < T::KSTEPS; ++ks)
+        for (int ks = 0; ks < D / 16; ++ks)
             qf[ks] = valid ? *(const u32x4 *)(qrow + 16 * ks + 8 * grp) : (u32x4){0, 0, 0, 0};
     }
 
@@ -243,14 +162,8 @@ void attn_bf16_kernel(const AttnParams p) {
     const uint32_t v_lane = (4 * (g16 >> 1) + (l16 >> 2)) * T::V_PITCH + (16 * (g16 & 1) + 4 * (l16 & 3)) * 2;
     const uint32_t k_lane = j * T::K_PITCH + 16 * grp;
 
-    // ---- running softmax state of this lane's row (log2 domain, scaled)
-    float m_run = -1e30f;
-    float l_run = 0.f;
-    f32x16 o_acc[T::DBLK];
-#pragma unroll
-    for (int mt = 0; mt < T::DBLK; ++mt)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) o_acc[mt][i] = 0.f;
+    RowState<D> rs;
+    rs.zero();
     const float c2 = p.scale_log2;
 
     const int ntiles = ke > kb ? (int)((ke - kb + BN - 1) / BN) : 0;
@@ -269,120 +182,21 @@ void attn_bf16_kernel(const AttnParams p) {
         if (wave_active) {
             const unsigned char *ks_ = smem + cur * T::STAGE;
             const unsigned char *vs_ = ks_ + T::K_BYTES;
-
-            // S^T for the two 32-key sub-tiles
-            f32x16 s[2];
-#pragma unroll
-            for (int st = 0; st < 2; ++st) {
-#pragma unroll
-                for (int i = 0; i < 16; ++i) s[st][i] = 0.f;
-#pragma unroll
-                for (int ks = 0; ks < T::KSTEPS; ++ks) {
-                    u32x4 a = *(const u32x4 *)(ks_ + k_lane + 32 * st * T::K_PITCH + 32 * ks);
-                    s[st] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a), as_bf16x8(qf[ks]), s[st], 0, 0, 0);
-                }
-            }
-            // causal mask: key k0 + 32*st + 8*(i/4) + 4*grp + i%4 is visible iff <= pos
-            if (k0 + BN > k_full) {
-                const int64_t lim64 = pos - k0;
-                const int lim = lim64 < -1 ? -1 : (lim64 > BN ? BN : (int)lim64);
-#pragma unroll
-                for (int st = 0; st < 2; ++st)
-#pragma unroll
-                    for (int i = 0; i < 16; ++i) {
-                        const int o = 32 * st + 8 * (i >> 2) + 4 * grp + (i & 3);
-                        if (o > lim) s[st][i] = -INFINITY;
-                    }
-            }
-            float mx = -INFINITY;
-#pragma unroll
-            for (int st = 0; st < 2; ++st)
-#pragma unroll
-                for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s[st][i]);
-            mx = pair_max(mx) * c2;
-            // lazy rescale: move the reference only when p could exceed 2^kRescaleSlack
-            const bool need = mx > m_run + kRescaleSlack;
-            if (__ballot(need)) {
-                const float m_new = need ? mx : m_run;
-                const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-                m_run = m_new;
-                l_run *= alpha;
-#pragma unroll
-                for (int mt = 0; mt < T::DBLK; ++mt)
-#pragma unroll
-                    for (int i = 0; i < 16; ++i) o_acc[mt][i] *= alpha;
-            }
-            float lsum = 0.f;
-            u32x4 pf[2][2];   // P^T as bf16, [sub-tile][16-key half]
-#pragma unroll
-            for (int st = 0; st < 2; ++st) {
-#pragma unroll
-                for (int i = 0; i < 16; i += 2) {
-                    const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[st][i], c2, -m_run));
-                    const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[st][i + 1], c2, -m_run));
-                    const uint32_t pk = pack_bf16x2(p0, p1);
-                    // normalise by the weights the PV product really uses (bf16-rounded):
-                    // the output is an exact convex combination of V rows
-                    lsum = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, pk), kOnes, lsum, false);
-                    pf[st][i >> 3][(i & 7) >> 1] = pk;
-                }
-            }
-            l_run += lsum;
-
-            // O^T += V^T P^T; P^T slot e of half kk is key 32*st + 16*kk + 8*(e/4) + 4*grp + e%4
-#pragma unroll
-            for (int st = 0; st < 2; ++st)
-#pragma unroll
-                for (int kk = 0; kk < 2; ++kk) {
-#pragma unroll
-                    for (int mt = 0; mt < T::DBLK; ++mt) {
-                        const unsigned char *va = vs_ + v_lane + (32 * st + 16 * kk) * T::V_PITCH + 64 * mt;
-                        i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)va);
-                        i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)(va + 8 * T::V_PITCH));
-                        u32x2 lo2 = __builtin_bit_cast(u32x2, lo);
-                        u32x2 hi2 = __builtin_bit_cast(u32x2, hi);
-                        u32x4 a = {lo2[0], lo2[1], hi2[0], hi2[1]};
-                        o_acc[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a), as_bf16x8(pf[st][kk]),
-                                                                           o_acc[mt], 0, 0, 0);
-                    }
-                }
+            const bool mask = k0 + BN > k_full;
+            const int64_t lim64 = pos - k0;
+            const int lim = lim64 < -1 ? -1 : (lim64 > BN ? BN : (int)lim64);
+            tile_step<D>(
+                rs, qf,
+                [&](int st, int ks) { return ks_ + k_lane + 32 * st * T::K_PITCH + 32 * ks; },
+                [&](int st, int kk, int h, int mt) {
+                    return vs_ + v_lane + (32 * st + 16 * kk + 8 * h) * T::V_PITCH + 64 * mt;
+                },
+                mask, lim, c2, grp);
         }
         if (more) swrite(cur ^ 1);
         __syncthreads();
     }
-
-    // ---- epilogue
-    const float l_tot = pair_sum(l_run);
-    if (!valid) return;
-    if (MODE != kModeContinue || p.nsplit == 1) {
-        const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
-        __bf16 *orow = (__bf16 *)p.out + ((int64_t)(tok0 + tok) * p.n_q_heads + head) * D;
-#pragma unroll
-        for (int mt = 0; mt < T::DBLK; ++mt)
-#pragma unroll
-            for (int q4 = 0; q4 < 4; ++q4) {
-                const int d = 32 * mt + 8 * q4 + 4 * grp;
-                u32x2 v;
-                v[0] = pack_bf16x2(o_acc[mt][4 * q4 + 0] * inv, o_acc[mt][4 * q4 + 1] * inv);
-                v[1] = pack_bf16x2(o_acc[mt][4 * q4 + 2] * inv, o_acc[mt][4 * q4 + 3] * inv);
-                *(u32x2 *)(orow + d) = v;
-            }
-    } else {
-        const int64_t prow = ((int64_t)split * p.n_kv_heads + g) * p.rows_total + r;
-        float *po = p.ws + prow * D;
-#pragma unroll
-        for (int mt = 0; mt < T::DBLK; ++mt)
-#pragma unroll
-            for (int q4 = 0; q4 < 4; ++q4) {
-                const int d = 32 * mt + 8 * q4 + 4 * grp;
-                *(float4 *)(po + d) = make_float4(o_acc[mt][4 * q4], o_acc[mt][4 * q4 + 1], o_acc[mt][4 * q4 + 2],
-                                                  o_acc[mt][4 * q4 + 3]);
-            }
-        if (grp == 0) {
-            float *pml = p.ws + (int64_t)p.nsplit * p.n_kv_heads * p.rows_total * D + prow * 2;
-            *(float2 *)pml = make_float2(m_run, l_tot);
-        }
-    }
+    epilogue<D, MODE>(p, w, rs, r, valid, tok, head, grp);
 }
 
 // Combine the per-split partial results (fixed split order, so the result is

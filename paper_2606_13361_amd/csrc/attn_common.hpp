@@ -1,0 +1,246 @@
+// attn_common.hpp -- device pieces shared by the two bf16 attention kernels
+// (register-staged tiles in attn_bf16.hip, direct-to-LDS streamed tiles in
+// attn_stream.hip): work-item decoding, the per-tile MFMA / online-softmax
+// step and the epilogue.
+//
+// Notation of one 64-key tile and one wave (32 query rows = MFMA columns):
+//   S^T[key][row] = K Q^T              v_mfma_f32_32x32x16_bf16, K from LDS,
+//                                      Q^T fragments held in registers
+//   online softmax in the log2 domain  a lane owns one query row and 16 keys
+//                                      of each 32-key sub-tile; lanes l and
+//                                      l^32 hold the two halves of a row
+//   O^T[d][row] += V^T P^T             V^T through the transposing LDS read,
+//                                      P^T = the score accumulator, rounded
+//                                      to bf16 in registers
+// The MFMA k-slots of P^T and V^T only have to name the same key: slot e of
+// 16-key half kk of sub-tile st is key 32*st + 16*kk + 8*(e/4) + 4*grp + e%4,
+// which is where the score accumulator left it.
+#pragma once
+
+#include "kvr_internal.hpp"
+
+namespace kvr {
+namespace dev {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+
+constexpr int BN = kKeyTile;     // keys per tile
+constexpr int ROWS = kRowsBf16;  // query rows per workgroup (4 waves x 32)
+constexpr int THREADS = 256;
+// The running row maximum is only moved when a tile's maximum exceeds it by
+// more than this (log2 units): p = 2^(s - m) then stays below 2^8, which bf16
+// P and fp32 sums hold as well as p <= 1, and the O rescale is skipped for
+// almost every tile.
+constexpr float kRescaleSlack = 8.f;
+
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+    // v_cvt_pk_bf16_f32: round to nearest even
+    bf16x2 v;
+    v[0] = (__bf16)lo;
+    v[1] = (__bf16)hi;
+    return __builtin_bit_cast(uint32_t, v);
+}
+
+__device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
+
+// Lanes l and l^32 hold the two halves of one query row.  v_permlane32_swap
+// exchanges the upper half of its first operand with the lower half of its
+// second; with both operands x the two results are {x[l], x[l^32]} in some
+// order, so their max / sum is the row's (and the same bits in both lanes).
+__device__ __forceinline__ float pair_max(float x) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float pair_sum(float x) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+// Locate the segment (reader) that owns a linear row-tile index.
+__device__ __forceinline__ int find_segment(const AttnParams &p, int tile) {
+    int lo = 0, hi = p.n_seg - 1;
+    while (lo < hi) {
+        int mid = (lo + hi + 1) >> 1;
+        if (p.seg_tile0[mid] <= tile) lo = mid; else hi = mid - 1;
+    }
+    return lo;
+}
+
+// What one workgroup computes: 128 rows (token-major (token, head) pairs of
+// kv head g) of one segment, over keys [kb, ke).
+struct Work {
+    int g, split, seg, tok0, n_tok, G, R, row0, row_last;
+    int64_t npre, kb, ke;
+};
+
+template <int MODE>
+__device__ __forceinline__ Work decode_work(const AttnParams &p) {
+    Work w;
+    int b = blockIdx.x;
+    // kv head fastest: consecutive workgroups land on different XCDs, so each
+    // XCD keeps one head's K/V rows in its L2
+    w.g = b % p.n_kv_heads;
+    b /= p.n_kv_heads;
+    w.split = b % p.nsplit;
+    b /= p.nsplit;
+    const int tile_lin = MODE == kModePrefill ? (p.tiles_total - 1 - b) : b;   // longest rows first
+    w.seg = MODE == kModeReaders ? find_segment(p, tile_lin) : 0;
+    const int rt = tile_lin - p.seg_tile0[w.seg];
+    w.tok0 = p.seg_tok0[w.seg];
+    w.n_tok = p.seg_tok0[w.seg + 1] - w.tok0;
+    w.G = p.group;
+    w.R = w.G * w.n_tok;
+    w.row0 = rt * ROWS;
+    w.row_last = min(w.row0 + ROWS, w.R) - 1;
+    w.npre = MODE == kModePrefill ? 0 : p.n_prefix;
+    const int64_t k_all = w.npre + w.row_last / w.G + 1;   // keys any row of the workgroup may see
+    w.kb = 0;
+    w.ke = k_all;
+    if (MODE == kModeContinue && p.nsplit > 1) {
+        w.kb = (int64_t)w.split * p.chunk;
+        w.ke = (w.split == p.nsplit - 1) ? k_all : min(w.kb + p.chunk, w.npre);
+    }
+    return w;
+}
+
+// Running softmax state of one lane's query row (log2 domain, scaled).
+template <int D>
+struct RowState {
+    f32x16 o[D / 32];
+    float m = -1e30f;
+    float l = 0.f;
+    __device__ __forceinline__ void zero() {
+#pragma unroll
+        for (int mt = 0; mt < D / 32; ++mt)
+#pragma unroll
+            for (int i = 0; i < 16; ++i) o[mt][i] = 0.f;
+    }
+};
+
+__device__ const bf16x2 kOnes = {(__bf16)1.0f, (__bf16)1.0f};
+
+// One tile of 32 * NSUB keys for one wave.
+//   kaddr(st, ks)         LDS byte address of this lane's K fragment (row 32*st + j,
+//                         head-dim slots 16*ks + 8*grp .. +7)
+//   vaddr(st, kk, h, mt)  LDS byte address this lane passes to the transposing
+//                         read for keys 32*st + 16*kk + 8*h + 4*(g16/2) .. +3
+//   lim                   keys with tile offset > lim are masked (only if mask)
+template <int D, int NSUB = 2, class KA, class VA>
+__device__ __forceinline__ void tile_step(RowState<D> &rs, const u32x4 (&qf)[D / 16], KA kaddr, VA vaddr,
+                                          bool mask, int lim, float c2, int grp) {
+    f32x16 s[NSUB];
+#pragma unroll
+    for (int st = 0; st < NSUB; ++st) {
+#pragma unroll
+        for (int i = 0; i < 16; ++i) s[st][i] = 0.f;
+#pragma unroll
+        for (int ks = 0; ks < D / 16; ++ks) {
+            const u32x4 a = *(const u32x4 *)kaddr(st, ks);
+            s[st] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a), as_bf16x8(qf[ks]), s[st], 0, 0, 0);
+        }
+    }
+    // causal mask: tile key offset 32*st + 8*(i/4) + 4*grp + i%4 is visible iff <= lim
+    if (mask) {
+#pragma unroll
+        for (int st = 0; st < NSUB; ++st)
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+                const int o = 32 * st + 8 * (i >> 2) + 4 * grp + (i & 3);
+                if (o > lim) s[st][i] = -INFINITY;
+            }
+    }
+    float mx = -INFINITY;
+#pragma unroll
+    for (int st = 0; st < NSUB; ++st)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s[st][i]);
+    mx = pair_max(mx) * c2;
+    // lazy rescale: move the reference only when p could exceed 2^kRescaleSlack
+    const bool need = mx > rs.m + kRescaleSlack;
+    if (__ballot(need)) {
+        const float m_new = need ? mx : rs.m;
+        const float alpha = __builtin_amdgcn_exp2f(rs.m - m_new);
+        rs.m = m_new;
+        rs.l *= alpha;
+#pragma unroll
+        for (int mt = 0; mt < D / 32; ++mt)
+#pragma unroll
+            for (int i = 0; i < 16; ++i) rs.o[mt][i] *= alpha;
+    }
+    float lsum = 0.f;
+    u32x4 pf[NSUB][2];   // P^T as bf16, [sub-tile][16-key half]
+#pragma unroll
+    for (int st = 0; st < NSUB; ++st) {
+#pragma unroll
+        for (int i = 0; i < 16; i += 2) {
+            const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[st][i], c2, -rs.m));
+            const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[st][i + 1], c2, -rs.m));
+            const uint32_t pk = pack_bf16x2(p0, p1);
+            // normalise by the weights the PV product really uses (bf16-rounded):
+            // the output is an exact convex combination of V rows
+            lsum = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, pk), kOnes, lsum, false);
+            pf[st][i >> 3][(i & 7) >> 1] = pk;
+        }
+    }
+    rs.l += lsum;
+#pragma unroll
+    for (int st = 0; st < NSUB; ++st)
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+            for (int mt = 0; mt < D / 32; ++mt) {
+                const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)vaddr(st, kk, 0, mt));
+                const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)vaddr(st, kk, 1, mt));
+                const u32x2 lo2 = __builtin_bit_cast(u32x2, lo);
+                const u32x2 hi2 = __builtin_bit_cast(u32x2, hi);
+                const u32x4 a = {lo2[0], lo2[1], hi2[0], hi2[1]};
+                rs.o[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a), as_bf16x8(pf[st][kk]), rs.o[mt],
+                                                                  0, 0, 0);
+            }
+}
+
+// Final output (normalised, bf16) or split partial (unnormalised O, m, l).
+template <int D, int MODE>
+__device__ __forceinline__ void epilogue(const AttnParams &p, const Work &w, const RowState<D> &rs, int r,
+                                         bool valid, int tok, int head, int grp) {
+    const float l_tot = pair_sum(rs.l);
+    if (!valid) return;
+    if (MODE != kModeContinue || p.nsplit == 1) {
+        const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+        __bf16 *orow = (__bf16 *)p.out + ((int64_t)(w.tok0 + tok) * p.n_q_heads + head) * D;
+#pragma unroll
+        for (int mt = 0; mt < D / 32; ++mt)
+#pragma unroll
+            for (int q4 = 0; q4 < 4; ++q4) {
+                const int d = 32 * mt + 8 * q4 + 4 * grp;
+                u32x2 v;
+                v[0] = pack_bf16x2(rs.o[mt][4 * q4 + 0] * inv, rs.o[mt][4 * q4 + 1] * inv);
+                v[1] = pack_bf16x2(rs.o[mt][4 * q4 + 2] * inv, rs.o[mt][4 * q4 + 3] * inv);
+                *(u32x2 *)(orow + d) = v;
+            }
+    } else {
+        const int64_t prow = ((int64_t)w.split * p.n_kv_heads + w.g) * p.rows_total + r;
+        float *po = p.ws + prow * D;
+#pragma unroll
+        for (int mt = 0; mt < D / 32; ++mt)
+#pragma unroll
+            for (int q4 = 0; q4 < 4; ++q4) {
+                const int d = 32 * mt + 8 * q4 + 4 * grp;
+                *(float4 *)(po + d) = make_float4(rs.o[mt][4 * q4], rs.o[mt][4 * q4 + 1], rs.o[mt][4 * q4 + 2],
+                                                  rs.o[mt][4 * q4 + 3]);
+            }
+        if (grp == 0) {
+            float *pml = p.ws + (int64_t)p.nsplit * p.n_kv_heads * p.rows_total * D + prow * 2;
+            *(float2 *)pml = make_float2(rs.m, l_tot);
+        }
+    }
+}
+
+}  // namespace dev
+}  // namespace kvr

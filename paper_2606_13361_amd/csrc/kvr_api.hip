@@ -14,9 +14,13 @@ namespace {
 constexpr int64_t kMaxTokens = (int64_t)1 << 30;   // rows of Q per call; keeps int32 row math safe
 constexpr int64_t kMaxKeys = (int64_t)1 << 40;
 // Split heuristic for the continuation: aim for this many workgroups on the
-// 256-CU part, never split the prefix below this many keys per workgroup.
-constexpr int64_t kTargetWorkgroups = 512;
+// 256-CU part (two per CU for both kernels), never split the prefix below
+// this many keys per workgroup.
+constexpr int64_t kTargetWorkgroupsStaged = 512;
 constexpr int64_t kMinSplitKeys = 256;
+
+// The streamed kernel serves bf16, head_dim 128 many-readers calls.
+bool use_stream(const kvr_desc *d) { return d->dtype == KVR_BF16 && d->head_dim == 128; }
 
 bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
 
@@ -53,8 +57,9 @@ Split plan_split(const kvr_desc *d, int64_t L_prefix, int64_t S) {
     const int64_t rows = G * S;
     const int64_t tiles = (rows + kRowsBf16 - 1) / kRowsBf16;
     const int64_t base = tiles * d->n_kv_heads;
-    if (base >= kTargetWorkgroups) return s;
-    int64_t want = (kTargetWorkgroups + base - 1) / base;
+    const int64_t target = kTargetWorkgroupsStaged;
+    if (base >= target) return s;
+    int64_t want = (target + base - 1) / base;
     const int64_t most = (L_prefix + kMinSplitKeys - 1) / kMinSplitKeys;
     if (want > most) want = most;
     if (want > kMaxSplits) want = kMaxSplits;
@@ -267,8 +272,9 @@ int kvr_continue_batched(const kvr_desc *desc, const void *Qs, const void *Ks, c
         p.tiles_total = tiles;
         p.rows_total = 0;
         const int64_t grid = (int64_t)tiles * p.n_kv_heads;
-        hipError_t e = desc->dtype == KVR_BF16 ? launch_attn_bf16(p, desc->head_dim, kModeReaders, (int)grid,
-                                                                  (hipStream_t)stream)
+        hipError_t e = use_stream(desc) ? launch_attn_stream(p, kModeReaders, (int)grid, (hipStream_t)stream)
+                       : desc->dtype == KVR_BF16 ? launch_attn_bf16(p, desc->head_dim, kModeReaders, (int)grid,
+                                                                    (hipStream_t)stream)
                                                : launch_attn_f32(p, desc->head_dim, (int)grid, (hipStream_t)stream);
         if (e != hipSuccess) return KVR_ERR_DEVICE;
     }

@@ -60,6 +60,12 @@ enum { kModePrefill = 0, kModeContinue = 1, kModeReaders = 2 };
 // bf16 path (MFMA), D in {64, 128}
 hipError_t launch_attn_bf16(const AttnParams &p, int head_dim, int mode, int grid, hipStream_t s);
 hipError_t launch_merge_bf16(const MergeParams &p, int head_dim, hipStream_t s);
+// bf16 streamed path (direct-to-LDS tile pipeline), D = 128, continue / readers
+constexpr int kStreamStagesContinue = 4;   // x 32 keys (16 KB): 64 KB of LDS, two workgroups per CU
+constexpr int kStreamSubContinue = 1;
+constexpr int kStreamStagesReaders = 2;    // x 64 keys (32 KB): 64 KB of LDS, two workgroups per CU
+constexpr int kStreamSubReaders = 2;
+hipError_t launch_attn_stream(const AttnParams &p, int mode, int grid, hipStream_t s);
 // fp32 path (VALU), D in {64, 128}
 hipError_t launch_attn_f32(const AttnParams &p, int head_dim, int grid, hipStream_t s);
 // cache write

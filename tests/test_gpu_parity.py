@@ -51,6 +51,21 @@ def gpu_continue(d, qs, ks, vs, kc, vc, Lp):
     return out
 
 
+def claim1(a, b, dtype=torch.bfloat16):
+    """Continuation rows vs prefill rows, both from the GPU.
+
+    2e-3 on the workloads' scale; each bf16 result is also rounded to the
+    output format on its own, so two different summation orders may land on
+    neighbouring bf16 values: one output ulp (|x| * 2^-7) is allowed on top
+    (it matters only where outputs exceed ~0.25, i.e. short contexts).
+    """
+    a = a.double().cpu()
+    b = b.double().cpu()
+    rel = 2.0 ** -7 if dtype == torch.bfloat16 else 0.0
+    worst = float(((a - b).abs() - (CLAIM1_TOL + rel * b.abs())).max())
+    assert worst <= 0.0, worst
+
+
 def maxabs(gpu, want):
     return float(np.max(np.abs(gpu.float().cpu().numpy().astype(np.float64) - want))) if want.size else 0.0
 
@@ -124,7 +139,7 @@ def test_continue_bf16_vs_oracle_and_prefill(Lp, S):
         d = kvr.make_desc(32, 8, 128, torch.bfloat16, 0)
     cont = gpu_continue(d, q[Lp:], k[Lp:], v[Lp:], kc, vc, Lp)
     torch.cuda.synchronize()
-    assert float((cont - full[Lp:]).abs().max()) <= CLAIM1_TOL
+    claim1(cont, full[Lp:])
     kc_o = k[:Lp].transpose(0, 1).contiguous() if Lp else torch.zeros((8, 0, 128), dtype=torch.bfloat16)
     vc_o = v[:Lp].transpose(0, 1).contiguous() if Lp else torch.zeros((8, 0, 128), dtype=torch.bfloat16)
     want, _ = ref.continue_(q[Lp:], k[Lp:], v[Lp:], kc_o, vc_o, Lp)
@@ -223,7 +238,7 @@ def test_decode_chain():
         outs.append(o)
     torch.cuda.synchronize()
     chain = torch.cat(outs)
-    assert float((chain - full[L:]).abs().max()) <= CLAIM1_TOL
+    claim1(chain, full[L:])
     want, _ = ref.prefill(q, k, v, rows=list(range(L, L + T)))
     assert maxabs(chain, want) <= TOL[torch.bfloat16]
 
@@ -256,7 +271,7 @@ def test_many_readers_batched():
         a, b = cu[r], cu[r + 1]
         single = gpu_continue(d, qs[a:b], ks[a:b], vs[a:b], kc, vc, Lp)
         torch.cuda.synchronize()
-        assert float((single - out[a:b]).abs().max()) <= CLAIM1_TOL
+        claim1(single, out[a:b])
 
 
 def test_shifted_failure_mode():
