@@ -45,6 +45,8 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="target CPU-oracle sample time")
     ap.add_argument("--sweep-lengths", type=str, default=None,
                     help="comma-separated prefix lengths for the sweep (default: all four)")
+    ap.add_argument("--sweep-suffix", type=int, default=None,
+                    help="suffix length S of the sweep continuations (default 24)")
     ap.add_argument("--sweep-only", action="store_true",
                     help="skip the layer step (for profiling one sweep length)")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -127,7 +129,7 @@ def main():
     if args.sweep_only:
         res = {"sweep": sweep(torch, kvr, A, W, dev, stream,
                               [int(x) for x in args.sweep_lengths.split(",")] if args.sweep_lengths
-                              else list(W.SWEEP_L))}
+                              else list(W.SWEEP_L), args.sweep_suffix)}
         print(json.dumps(res), flush=True)
         return
 
@@ -213,12 +215,36 @@ def main():
 
     if not args.no_sweep:
         lens_ = [int(x) for x in args.sweep_lengths.split(",")] if args.sweep_lengths else list(W.SWEEP_L)
-        result["sweep"] = sweep(torch, kvr, A, W, dev, stream, lens_)
+        result["sweep"] = sweep(torch, kvr, A, W, dev, stream, lens_, args.sweep_suffix)
     if not args.no_decode36:
         result["decode36"] = decode36(torch, kvr, A, W, dev, stream)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(q, k, v, A, args.cpu_seconds)
     print(json.dumps(result), flush=True)
+
+
+def graph_time(torch, stream, issue, n_calls, replays=5):
+    """Seconds per call of `issue()` (which issues n_calls calls) captured in a HIP graph and replayed."""
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        issue()                       # warm up on the capture stream
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        issue()
+    g.replay()
+    torch.cuda.synchronize()
+    cur = torch.cuda.current_stream()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record(cur)
+    for _ in range(replays):
+        g.replay()
+    b.record(cur)
+    torch.cuda.synchronize()
+    del g
+    return a.elapsed_time(b) * 1e-3 / (replays * n_calls)
 
 
 def timed(torch, stream, fn, iters):
@@ -231,11 +257,11 @@ def timed(torch, stream, fn, iters):
     return [ev[i].elapsed_time(ev[i + 1]) * 1e-3 for i in range(iters)]
 
 
-def sweep(torch, kvr, A, W, dev, stream, lengths):
+def sweep(torch, kvr, A, W, dev, stream, lengths, suffix=None):
     """Prefill of L+24 vs continuation of 24 over L, L in {1024, 4096, 16384, 32768}."""
     sh = W.QWEN
     Hq, Hkv, D = sh.n_q_heads, sh.n_kv_heads, sh.head_dim
-    S = W.SWEEP_S
+    S = suffix or W.SWEEP_S
     rows = []
     for L in lengths:
         n = L + S
@@ -262,10 +288,19 @@ def sweep(torch, kvr, A, W, dev, stream, lengths):
             kvr.kvr_continue(desc, qs, ks, vs, c[0], c[1], L, S, oc, ws)
         for i in range(R):
             cont(i)
-        tc = timed(torch, stream, cont, iters)
+        tc_eager = timed(torch, stream, cont, iters)
+        # GPU time without host launch overhead: the R calls captured in one HIP
+        # graph, replayed; the last replay's output must equal the eager one bit for bit
+        cont(R - 1)
+        torch.cuda.synchronize()
+        ref_out = oc.clone()
+        tc = graph_time(torch, stream, lambda: [cont(i) for i in range(R)], R)
+        if not torch.equal(oc, ref_out):
+            raise RuntimeError("graph replay of the continuation differs from the eager result")
         del pool
         tp_avg = sum(tp) / len(tp)
-        tc_avg = sum(tc) / len(tc)
+        tc_avg = tc
+        tce_avg = sum(tc_eager) / len(tc_eager)
         fl = A.prefill_flops(n, Hq, D)
         by = A.continue_bytes(L, S, Hq, Hkv, D, 2)
         rows.append({
@@ -277,6 +312,8 @@ def sweep(torch, kvr, A, W, dev, stream, lengths):
             "continue_GBps": round(by / tc_avg / 1e9, 1),
             "continue_hbm_frac": round(by / tc_avg / 1e9 / PEAK_HBM_GBPS, 4),
             "continue_rotated_caches": R,
+            "continue_eager_us": round(tce_avg * 1e6, 2),
+            "continue_timing": "HIP-graph replay of %d rotated calls (eager: host-issued, one event pair per call)" % R,
             "reuse_speedup": round(tp_avg / tc_avg, 2),
             "break_even_N": round(A.break_even(tp_avg, tc_avg), 4),
         })
@@ -314,17 +351,21 @@ def decode36(torch, kvr, A, W, dev, stream):
     run_chain()
     torch.cuda.synchronize()
     ts = timed(torch, stream, lambda i: run_chain(), 3)
-    t_avg = sum(ts) / len(ts)
+    t_eager = sum(ts) / len(ts)
+    # the whole chain (864 continue + 864 append calls) as one HIP graph
+    t_avg = graph_time(torch, stream, run_chain, 1, replays=3)
     by = sum(A.continue_bytes(Lz + t, 1, Hq, Hkv, D, 2) + A.append_bytes(1, Hkv, D, 2)
              for t in range(T)) * NL
     res = {
         "layers": NL, "prefix": Lz, "steps": T,
         "chain_ms": round(t_avg * 1e3, 3),
+        "chain_eager_ms": round(t_eager * 1e3, 3),
         "per_call_us": round(t_avg / (T * NL) * 1e6, 2),
         "GBps": round(by / t_avg / 1e9, 1),
         "hbm_frac": round(by / t_avg / 1e9 / PEAK_HBM_GBPS, 4),
         "resident_cache_GB": round(caches.numel() * 2 / 1e9, 3),
-        "note": "host-issued launches (continue + append per layer per step), end-to-end",
+        "note": "continue + append per layer per step; timed as one HIP-graph replay of the chain "
+                "(chain_eager_ms: host-issued launches)",
     }
     del caches, qkv
     torch.cuda.empty_cache()

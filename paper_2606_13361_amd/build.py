@@ -18,6 +18,9 @@ HIPCC_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
     # no packed fp32 instructions in any generated code
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # MFMA accumulators in ordinary VGPRs: keeps the loop-carried attention
+    # accumulators out of AGPR <-> VGPR copies around the softmax updates
+    "-mllvm", "-amdgpu-mfma-vgpr-form",
 ]
 
 

@@ -43,7 +43,7 @@ void attn_bf16_kernel(const AttnParams p) {
     __shared__ __attribute__((aligned(16))) unsigned char smem[2 * T::STAGE];
 
     const int tid = threadIdx.x;
-    const int wave = tid >> 6;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform: scalar branches
     const int lane = tid & 63;
     const int j = lane & 31;      // query row (MFMA column) owned by this lane
     const int grp = lane >> 5;    // which half of each key quad-set this lane holds

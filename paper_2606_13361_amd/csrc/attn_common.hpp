@@ -125,6 +125,32 @@ struct RowState {
 
 __device__ const bf16x2 kOnes = {(__bf16)1.0f, (__bf16)1.0f};
 
+// Direct-to-LDS load of 16 bytes per lane: lane l's bytes land at LDS byte
+// lds + 16*l (lds is wave-uniform).  Issued as inline asm so the compiler does
+// not treat it as an LDS write it must wait for before every later LDS read
+// (it cannot tell pipeline stages apart and would drain all loads in flight);
+// the kernels wait for their own stages explicitly with wait_vmcnt, and order
+// these loads against the LDS reads of the slot they refill with compiler
+// fences (asm volatile statements keep their order among themselves).
+// m0 is named as clobbered: these kernels use it for nothing else (no LDS
+// DMA of the compiler's own, no indirect register indexing, no messages).
+__device__ __forceinline__ void dma16(const void *src, const void *lds_dst) {
+    const uint32_t lds = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void *)lds_dst;
+    asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(lds), "v"(src) : "m0");
+}
+
+// s_waitcnt with vmcnt = N and the other counters left alone (gfx9 encoding:
+// vmcnt[3:0] bits 3:0, expcnt bits 6:4, lgkmcnt bits 11:8, vmcnt[5:4] bits 15:14).
+// Vector memory loads complete in issue order, so vmcnt(N) means every load
+// but the last N issued has landed.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | (((N >> 4) & 3) << 14));
+    asm volatile("" ::: "memory");
+}
+
 // One tile of 32 * NSUB keys for one wave.
 //   kaddr(st, ks)         LDS byte address of this lane's K fragment (row 32*st + j,
 //                         head-dim slots 16*ks + 8*grp .. +7)

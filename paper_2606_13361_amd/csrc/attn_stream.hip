@@ -40,17 +40,6 @@ struct Stage {
 
 __device__ __forceinline__ int swz(int row) { return ((row >> 2) & 3) | ((row & 3) << 2); }
 
-// s_waitcnt with vmcnt = n and the other counters left alone (gfx9 encoding:
-// vmcnt[3:0] bits 3:0, expcnt bits 6:4, lgkmcnt bits 11:8, vmcnt[5:4] bits 15:14)
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-    static_assert(N >= 0 && N < 64, "vmcnt range");
-    __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | (((N >> 4) & 3) << 14));
-}
-
-__device__ __forceinline__ void dma16(const void *src, unsigned char *lds_dst) {
-    __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void *)lds_dst, 16, 0, 0);
-}
 
 template <int NSTAGE, int NSUB, int MODE>
 __device__ __forceinline__ void stream_body(const AttnParams &p) {
@@ -61,7 +50,7 @@ __device__ __forceinline__ void stream_body(const AttnParams &p) {
     __shared__ __attribute__((aligned(1024))) unsigned char smem[NSTAGE * SG::BYTES];
 
     const int tid = threadIdx.x;
-    const int wave = tid >> 6;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform: scalar branches
     const int lane = tid & 63;
     const int j = lane & 31;
     const int grp = lane >> 5;
@@ -106,21 +95,26 @@ __device__ __forceinline__ void stream_body(const AttnParams &p) {
         off_n[i] = (uint32_t)(lrow[i] * nstride_b) + lchunk[i];
     }
     const int64_t cache_end = ke < npre ? ke : npre;
-    auto load_tile = [&](int64_t k0, int stage) {
-        unsigned char *kd = smem + stage * SG::BYTES + SG::ROWS_PER_WAVE * wave * ROW_BYTES;
-        unsigned char *vd = kd + SG::TILE_BYTES;
+    // addresses as integers: no pointer selects, nothing left in private memory
+    const uint64_t kc_a = (uint64_t)(uintptr_t)kc0, vc_a = (uint64_t)(uintptr_t)vc0;
+    const uint64_t kn_a = (uint64_t)(uintptr_t)kn0, vn_a = (uint64_t)(uintptr_t)vn0;
+    const uint32_t wave_lds = (uint32_t)(SG::ROWS_PER_WAVE * wave * ROW_BYTES);
+    auto load_tile = [=](int64_t k0, int stage) {
+        const unsigned char *kd = smem + stage * SG::BYTES + wave_lds;
+        const unsigned char *vd = kd + SG::TILE_BYTES;
         if (k0 + KEYS <= cache_end) {                     // all rows cached
-            const unsigned char *kb_ = kc0 + k0 * ROW_BYTES, *vb_ = vc0 + k0 * ROW_BYTES;
+            const uint64_t kb_ = kc_a + (uint64_t)k0 * ROW_BYTES, vb_ = vc_a + (uint64_t)k0 * ROW_BYTES;
 #pragma unroll
-            for (int i = 0; i < NL; ++i) dma16(kb_ + off_c[i], kd + 1024 * i);
+            for (int i = 0; i < NL; ++i) dma16((const void *)(kb_ + off_c[i]), kd + 1024 * i);
 #pragma unroll
-            for (int i = 0; i < NL; ++i) dma16(vb_ + off_c[i], vd + 1024 * i);
+            for (int i = 0; i < NL; ++i) dma16((const void *)(vb_ + off_c[i]), vd + 1024 * i);
         } else if (k0 >= npre && k0 + KEYS <= ke) {       // all rows new
-            const unsigned char *kb_ = kn0 + (k0 - npre) * nstride_b, *vb_ = vn0 + (k0 - npre) * nstride_b;
+            const uint64_t kb_ = kn_a + (uint64_t)(k0 - npre) * (uint64_t)nstride_b;
+            const uint64_t vb_ = vn_a + (uint64_t)(k0 - npre) * (uint64_t)nstride_b;
 #pragma unroll
-            for (int i = 0; i < NL; ++i) dma16(kb_ + off_n[i], kd + 1024 * i);
+            for (int i = 0; i < NL; ++i) dma16((const void *)(kb_ + off_n[i]), kd + 1024 * i);
 #pragma unroll
-            for (int i = 0; i < NL; ++i) dma16(vb_ + off_n[i], vd + 1024 * i);
+            for (int i = 0; i < NL; ++i) dma16((const void *)(vb_ + off_n[i]), vd + 1024 * i);
         } else {
             // mixed or ragged stage: rows past ke clamp to a valid row (beyond every
             // row's causal bound, masked, never counted)
@@ -129,9 +123,9 @@ __device__ __forceinline__ void stream_body(const AttnParams &p) {
                 const int64_t key = k0 + lrow[i];
                 const int64_t kk = key < ke ? key : ke - 1;
                 const bool in_cache = kk < npre;
-                const int64_t off = in_cache ? kk * ROW_BYTES : (kk - npre) * nstride_b;
-                dma16((in_cache ? kc0 : kn0) + off + lchunk[i], kd + 1024 * i);
-                dma16((in_cache ? vc0 : vn0) + off + lchunk[i], vd + 1024 * i);
+                const uint64_t off = in_cache ? (uint64_t)kk * ROW_BYTES : (uint64_t)(kk - npre) * (uint64_t)nstride_b;
+                dma16((const void *)((in_cache ? kc_a : kn_a) + off + lchunk[i]), kd + 1024 * i);
+                dma16((const void *)((in_cache ? vc_a : vn_a) + off + lchunk[i]), vd + 1024 * i);
             }
         }
     };

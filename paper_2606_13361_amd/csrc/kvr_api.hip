@@ -17,10 +17,17 @@ constexpr int64_t kMaxKeys = (int64_t)1 << 40;
 // 256-CU part (two per CU for both kernels), never split the prefix below
 // this many keys per workgroup.
 constexpr int64_t kTargetWorkgroupsStaged = 512;
+constexpr int64_t kTargetWorkgroupsCont = 256;   // split-K-in-workgroup kernel: one per CU (155 KB of LDS)
 constexpr int64_t kMinSplitKeys = 256;
 
 // The streamed kernel serves bf16, head_dim 128 many-readers calls.
 bool use_stream(const kvr_desc *d) { return d->dtype == KVR_BF16 && d->head_dim == 128; }
+
+// Continuations of at most kContMaxRows query rows per kv head (decode steps,
+// short suffixes) at bf16 / head_dim 128 use the kernel whose waves split the keys.
+bool use_cont(const kvr_desc *d, int64_t S) {
+    return d->dtype == KVR_BF16 && d->head_dim == 128 && (int64_t)(d->n_q_heads / d->n_kv_heads) * S <= kContMaxRows;
+}
 
 bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
 
@@ -57,7 +64,7 @@ Split plan_split(const kvr_desc *d, int64_t L_prefix, int64_t S) {
     const int64_t rows = G * S;
     const int64_t tiles = (rows + kRowsBf16 - 1) / kRowsBf16;
     const int64_t base = tiles * d->n_kv_heads;
-    const int64_t target = kTargetWorkgroupsStaged;
+    const int64_t target = use_cont(d, S) ? kTargetWorkgroupsCont : kTargetWorkgroupsStaged;
     if (base >= target) return s;
     int64_t want = (target + base - 1) / base;
     const int64_t most = (L_prefix + kMinSplitKeys - 1) / kMinSplitKeys;
@@ -137,7 +144,10 @@ int launch_single(const kvr_desc *d, int mode, const void *Q, const void *K, con
     if (grid <= 0) return KVR_OK;
     if (grid > 0x7fffffff) return KVR_ERR_SHAPE;
     hipError_t e;
-    if (d->dtype == KVR_BF16) {
+    if (mode == kModeContinue && use_cont(d, n_tok)) {
+        const int nct = (int)((rows + 31) / 32);
+        e = launch_attn_cont(p, nct, (int)grid, stream);
+    } else if (d->dtype == KVR_BF16) {
         e = launch_attn_bf16(p, d->head_dim, mode, (int)grid, stream);
     } else {
         if (mode == kModePrefill) {   // the fp32 kernel does not write the cache itself

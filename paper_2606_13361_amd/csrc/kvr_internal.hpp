@@ -66,6 +66,9 @@ constexpr int kStreamSubContinue = 1;
 constexpr int kStreamStagesReaders = 2;    // x 64 keys (32 KB): 64 KB of LDS, two workgroups per CU
 constexpr int kStreamSubReaders = 2;
 hipError_t launch_attn_stream(const AttnParams &p, int mode, int grid, hipStream_t s);
+// bf16 continuation for G*S <= 96 rows (D = 128): waves split the keys
+constexpr int kContMaxRows = 96;
+hipError_t launch_attn_cont(const AttnParams &p, int ncol_tiles, int grid, hipStream_t s);
 // fp32 path (VALU), D in {64, 128}
 hipError_t launch_attn_f32(const AttnParams &p, int head_dim, int grid, hipStream_t s);
 // cache write
