@@ -199,78 +199,6 @@ void attn_bf16_kernel(const AttnParams p) {
     epilogue<D, MODE>(p, w, rs, r, valid, tok, head, grp);
 }
 
-// Combine the per-split partial results (fixed split order, so the result is
-// reproducible bit for bit):
-//   M = max_s m_s,  w_s = 2^(m_s - M),  out = sum_s w_s O_s / sum_s w_s l_s
-// Workgroup = 32 rows of one kv head x one 32-wide slice of the head dim:
-// 256 lanes, 8 per row, each owning 4 consecutive head-dim values (16-byte
-// loads).  The per-split weights of the 32 rows are computed once, 8 lanes
-// per row, into LDS.
-constexpr int MERGE_ROWS = 32;
-constexpr int MERGE_DSLICE = 32;
-constexpr int MERGE_THREADS = MERGE_ROWS * MERGE_DSLICE / 4;
-
-template <int D>
-__global__ __launch_bounds__(MERGE_THREADS) void merge_bf16_kernel(const MergeParams p) {
-    constexpr int LPR = MERGE_DSLICE / 4;          // lanes per row (8)
-    constexpr int NSL = D / MERGE_DSLICE;          // head-dim slices
-    __shared__ float wts[kMaxSplits][MERGE_ROWS];
-    __shared__ float inv_l[MERGE_ROWS];
-    const int tid = threadIdx.x;
-    const int rr = tid / LPR;                      // row within the workgroup
-    const int part = tid % LPR;
-    const int tiles_per_head = (p.rows + MERGE_ROWS - 1) / MERGE_ROWS;
-    int b = blockIdx.x;
-    const int slice = b % NSL;
-    b /= NSL;
-    const int g = b / tiles_per_head;
-    const int r0 = (b % tiles_per_head) * MERGE_ROWS;
-    const int r = r0 + rr;
-    const bool valid = r < p.rows;
-    const int64_t per_split = (int64_t)p.n_kv_heads * p.rows;
-    const float *ml = p.ws + (int64_t)p.nsplit * per_split * D;
-    const int64_t row = (int64_t)g * p.rows + (valid ? r : r0);
-
-    // per-split weights: lane `part` of the row takes splits part, part+8, ...
-    float M = -INFINITY;
-    for (int s = part; s < p.nsplit; s += LPR) M = fmaxf(M, ml[(s * per_split + row) * 2]);
-    M = fmaxf(M, __shfl_xor(M, 1));
-    M = fmaxf(M, __shfl_xor(M, 2));
-    M = fmaxf(M, __shfl_xor(M, 4));
-    float l = 0.f;
-    for (int s = part; s < p.nsplit; s += LPR) {
-        const float2 v = *(const float2 *)(ml + (s * per_split + row) * 2);
-        const float w = __builtin_amdgcn_exp2f(v.x - M);
-        wts[s][rr] = w;
-        l += w * v.y;
-    }
-    // fixed-order reduction of the 8 partial sums (same in every lane)
-    l += __shfl_xor(l, 1);
-    l += __shfl_xor(l, 2);
-    l += __shfl_xor(l, 4);
-    if (part == 0) inv_l[rr] = l > 0.f ? 1.f / l : 0.f;
-    __syncthreads();
-    if (!valid) return;
-
-    const int d = slice * MERGE_DSLICE + 4 * part;
-    const float *src = p.ws + row * D + d;
-    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-#pragma unroll 8
-    for (int s = 0; s < p.nsplit; ++s) {
-        const float4 o = *(const float4 *)(src + s * per_split * D);
-        const float w = wts[s][rr];
-        acc.x += w * o.x; acc.y += w * o.y; acc.z += w * o.z; acc.w += w * o.w;
-    }
-    const float il = inv_l[rr];
-    const int tok = r / p.group;
-    const int head = g * p.group + r % p.group;
-    __bf16 *out = (__bf16 *)p.out + ((int64_t)tok * p.n_q_heads + head) * D + d;
-    u32x2 v;
-    v[0] = pack_bf16x2(acc.x * il, acc.y * il);
-    v[1] = pack_bf16x2(acc.z * il, acc.w * il);
-    *(u32x2 *)out = v;
-}
-
 template <int D>
 hipError_t launch_d(const AttnParams &p, int mode, int grid, hipStream_t s) {
     switch (mode) {
@@ -293,14 +221,5 @@ hipError_t launch_attn_bf16(const AttnParams &p, int head_dim, int mode, int gri
     return head_dim == 128 ? launch_d<128>(p, mode, grid, s) : launch_d<64>(p, mode, grid, s);
 }
 
-hipError_t launch_merge_bf16(const MergeParams &p, int head_dim, hipStream_t s) {
-    const int tiles = (p.rows + MERGE_ROWS - 1) / MERGE_ROWS;
-    const int grid = tiles * p.n_kv_heads * (head_dim / MERGE_DSLICE);
-    if (head_dim == 128)
-        hipLaunchKernelGGL(merge_bf16_kernel<128>, dim3(grid), dim3(MERGE_THREADS), 0, s, p);
-    else
-        hipLaunchKernelGGL(merge_bf16_kernel<64>, dim3(grid), dim3(MERGE_THREADS), 0, s, p);
-    return hipGetLastError();
-}
 
 }  // namespace kvr

@@ -9,9 +9,14 @@
 // (global_load_lds_dwordx4) and waits only on its own loads, so there is no
 // workgroup barrier in the key loop.  Within a stage every K fragment and
 // every V^T fragment read from LDS feeds all column tiles (1..3 independent
-// MFMA accumulation chains).  At the end the 4 waves' (m, l, O) are merged in
-// LDS (max, rescale, two-round tree add, fixed order) and wave 0 writes the
-// workgroup's split partial -- or the output when there is no split.
+// MFMA accumulation chains).  The query rows reach LDS by the same direct
+// loads, issued together with each wave's first K/V stage.
+//
+// Merge with a single barrier: every wave posts its (m, l) and the three
+// head-dim quarters of O it does not own; wave w then owns quarter w, sums the
+// four contributions scaled to the common maximum in a fixed order, and
+// stores that quarter of the workgroup's split partial -- or of the output
+// when there is no split.
 //
 // LDS tile layout as in the streamed kernel: 256-byte rows, 16-byte chunk c of
 // row r in slot c ^ swz(r), conflict-free for the K reads and the
@@ -35,8 +40,91 @@ constexpr int RINGS = 4 * RING;              // 128 KB
 constexpr int QROWS = 96;                    // query rows held in LDS
 constexpr int LDS_BYTES = RINGS + QROWS * ROWB;   // + 24 KB of Q
 
+// merge buffers, reusing the rings and Q: O quarters [4 owners][3 sources][NCT][4][64 lanes]
+// as float4, then m and l [4 waves][NCT][64 lanes]
+template <int NCT> constexpr int obuf_bytes() { return 12 * NCT * 4 * 64 * 16; }
+template <int NCT> constexpr int merge_bytes() { return obuf_bytes<NCT>() + 2 * 4 * NCT * 64 * 4; }
+static_assert(merge_bytes<3>() <= LDS_BYTES, "merge buffers exceed the LDS allocation");
+
 __device__ __forceinline__ int swz(int row) { return ((row >> 2) & 3) | ((row & 3) << 2); }
 
+
+// Head-dim quarter MT of every column tile: the four waves' contributions,
+// each scaled by 2^(m_w - M) with M the largest m_w, summed in wave order
+// 0..3 (the owner's own quarter comes from its registers, the others from
+// LDS), then stored -- bf16 output rows when there is no split, else the
+// split partial O quarter and, from the owner of quarter 0, (M, l).
+template <int NCT, int MT>
+__device__ __forceinline__ void finish_quarter(const AttnParams &p, const RowState<D> (&rs)[NCT],
+                                               const float4 *obuf, const float *lbuf, const float *mbuf,
+                                               const bool (&valid)[NCT], const int (&tok)[NCT],
+                                               const int (&head)[NCT], int g, int split, int lane) {
+    const int j = lane & 31;
+    const int grp = lane >> 5;
+#pragma unroll
+    for (int c = 0; c < NCT; ++c) {
+        float mw[4], alpha[4];
+        float M = -INFINITY;
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+            mw[w] = mbuf[(w * NCT + c) * 64 + lane];
+            M = fmaxf(M, mw[w]);
+        }
+#pragma unroll
+        for (int w = 0; w < 4; ++w) alpha[w] = __builtin_amdgcn_exp2f(mw[w] - M);
+        float l = 0.f;
+#pragma unroll
+        for (int w = 0; w < 4; ++w) l = __builtin_fmaf(alpha[w], lbuf[(w * NCT + c) * 64 + lane], l);
+        const float l_tot = pair_sum(l);
+        float acc[16];
+#pragma unroll
+        for (int i = 0; i < 16; ++i) acc[i] = 0.f;
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+            float x[16];
+            if (w == MT) {
+#pragma unroll
+                for (int i = 0; i < 16; ++i) x[i] = rs[c].o[MT][i];
+            } else {
+                const int slot = 3 * MT + (w > MT ? w - 1 : w);
+#pragma unroll
+                for (int q4 = 0; q4 < 4; ++q4) {
+                    const float4 v = obuf[((slot * NCT + c) * 4 + q4) * 64 + lane];
+                    x[4 * q4] = v.x;
+                    x[4 * q4 + 1] = v.y;
+                    x[4 * q4 + 2] = v.z;
+                    x[4 * q4 + 3] = v.w;
+                }
+            }
+#pragma unroll
+            for (int i = 0; i < 16; ++i) acc[i] = __builtin_fmaf(alpha[w], x[i], acc[i]);
+        }
+        if (!valid[c]) continue;
+        const int r = 32 * c + j;
+        if (p.nsplit == 1) {
+            const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+            __bf16 *orow = (__bf16 *)p.out + ((int64_t)tok[c] * p.n_q_heads + head[c]) * D;
+#pragma unroll
+            for (int q4 = 0; q4 < 4; ++q4) {
+                u32x2 v;
+                v[0] = pack_bf16x2(acc[4 * q4] * inv, acc[4 * q4 + 1] * inv);
+                v[1] = pack_bf16x2(acc[4 * q4 + 2] * inv, acc[4 * q4 + 3] * inv);
+                *(u32x2 *)(orow + 32 * MT + 8 * q4 + 4 * grp) = v;
+            }
+        } else {
+            const int64_t prow = ((int64_t)split * p.n_kv_heads + g) * p.rows_total + r;
+            float *po = p.ws + prow * D;
+#pragma unroll
+            for (int q4 = 0; q4 < 4; ++q4)
+                *(float4 *)(po + 32 * MT + 8 * q4 + 4 * grp) =
+                    make_float4(acc[4 * q4], acc[4 * q4 + 1], acc[4 * q4 + 2], acc[4 * q4 + 3]);
+            if (MT == 0 && grp == 0) {
+                float *pml = p.ws + (int64_t)p.nsplit * p.n_kv_heads * p.rows_total * D + prow * 2;
+                *(float2 *)pml = make_float2(M, l_tot);
+            }
+        }
+    }
+}
 
 template <int NCT>
 __global__ __launch_bounds__(THREADS) void attn_cont_kernel(const AttnParams p) {
@@ -73,21 +161,6 @@ __global__ __launch_bounds__(THREADS) void attn_cont_kernel(const AttnParams p) 
         head[c] = g * G + (valid[c] ? r % G : 0);
         pos[c] = valid[c] ? npre + tok[c] : -1;
     }
-    // Q rows of all column tiles into LDS once (swizzled like K; rows past R are zero),
-    // shared by the 4 waves; Q^T fragments are read from there for every stage
-    unsigned char *qlds = smem + RINGS;
-    for (int idx = tid; idx < 32 * NCT * 16; idx += THREADS) {
-        const int row = idx >> 4, chunk = idx & 15;
-        u32x4 v = {0, 0, 0, 0};
-        if (row < R) {
-            const __bf16 *qrow =
-                (const __bf16 *)p.q + ((int64_t)(row / G) * p.n_q_heads + g * G + row % G) * D;
-            v = *(const u32x4 *)(qrow + 8 * chunk);
-        }
-        *(u32x4 *)(qlds + row * ROWB + 16 * (chunk ^ swz(row))) = v;
-    }
-    __syncthreads();
-
     // ---- this wave's stages and its load map (instruction i moves rows 4*i + lane/16)
     const int nst = ke > kb ? (int)((ke - kb + SKEYS - 1) / SKEYS) : 0;
     const int my_n = nst > wave ? (nst - wave + 3) / 4 : 0;
@@ -156,7 +229,32 @@ __global__ __launch_bounds__(THREADS) void attn_cont_kernel(const AttnParams p) 
     for (int c = 0; c < NCT; ++c) rs[c].zero();
     const float c2 = p.scale_log2;
 
-    if (my_n > 0) load_stage(0);
+    // Q rows of all column tiles into LDS (swizzled like K, rows past R repeat
+    // row R-1: their columns are computed and never stored), then this wave's
+    // first stage; Q is older than the stage in the wave's load queue
+    const unsigned char *qlds = smem + RINGS;
+    {
+        const uint64_t q_a = (uint64_t)(uintptr_t)p.q + (uint64_t)g * G * ROWB;
+        const uint64_t qtok_b = (uint64_t)p.n_q_heads * ROWB;
+#pragma unroll
+        for (int i = 0; i < 2 * NCT; ++i) {
+            const int base = 4 * (2 * NCT * wave + i);
+            const int row = base + (lane >> 4);
+            const int rr = row < R ? row : R - 1;
+            const uint64_t src = q_a + (uint64_t)(rr / G) * qtok_b + (uint64_t)(rr % G) * ROWB +
+                                 16u * (uint32_t)((lane & 15) ^ swz(row));
+            dma16((const void *)src, qlds + base * ROWB);
+        }
+    }
+    if (my_n > 0) {
+        load_stage(0);
+        wait_vmcnt<LOADS>();
+    } else {
+        wait_vmcnt<0>();
+    }
+    __builtin_amdgcn_s_barrier();       // all of Q is in LDS
+    asm volatile("" ::: "memory");
+
     for (int t = 0; t < my_n; ++t) {
         asm volatile("" ::: "memory");
         if (t + 1 < my_n) {
@@ -244,66 +342,36 @@ __global__ __launch_bounds__(THREADS) void attn_cont_kernel(const AttnParams p) 
             }
     }
 
-    // ---- merge the 4 waves (fixed order): M = max_w m_w, scale by 2^(m_w - M), tree-add
-    float *obuf = (float *)smem;                                // 2 x [NCT*64 regs][64 lanes]
-    float *lbuf = obuf + 2 * NCT * 64 * 64;                     // 2 x [NCT][64]
-    float *mbuf = lbuf + 2 * NCT * 64;                          // [4][NCT][32]
-    __syncthreads();                                            // every wave is done with its ring
-    if (grp == 0) {
-#pragma unroll
-        for (int c = 0; c < NCT; ++c) mbuf[(wave * NCT + c) * 32 + j] = rs[c].m;
-    }
-    __syncthreads();
+    // ---- merge: post (m, l) and the non-owned O quarters, one barrier, then
+    // wave w finishes head-dim quarter w
+    __syncthreads();                    // every wave is done with its ring and with Q
+    float4 *obuf = (float4 *)smem;
+    float *lbuf = (float *)(smem + obuf_bytes<NCT>());
+    float *mbuf = lbuf + 4 * NCT * 64;
 #pragma unroll
     for (int c = 0; c < NCT; ++c) {
-        float M = mbuf[(0 * NCT + c) * 32 + j];
-#pragma unroll
-        for (int w = 1; w < 4; ++w) M = fmaxf(M, mbuf[(w * NCT + c) * 32 + j]);
-        const float alpha = __builtin_amdgcn_exp2f(rs[c].m - M);
-        rs[c].m = M;
-        rs[c].l *= alpha;
-#pragma unroll
-        for (int mt = 0; mt < D / 32; ++mt)
-#pragma unroll
-            for (int i = 0; i < 16; ++i) rs[c].o[mt][i] *= alpha;
+        mbuf[(wave * NCT + c) * 64 + lane] = rs[c].m;
+        lbuf[(wave * NCT + c) * 64 + lane] = rs[c].l;
     }
-    auto put = [&](int slot) {
 #pragma unroll
-        for (int c = 0; c < NCT; ++c) {
+    for (int mt = 0; mt < D / 32; ++mt) {
+        if (mt == wave) continue;
+        const int slot = 3 * mt + (wave > mt ? wave - 1 : wave);
 #pragma unroll
-            for (int mt = 0; mt < D / 32; ++mt)
+        for (int c = 0; c < NCT; ++c)
 #pragma unroll
-                for (int i = 0; i < 16; ++i)
-                    obuf[((slot * NCT + c) * 64 + mt * 16 + i) * 64 + lane] = rs[c].o[mt][i];
-            lbuf[(slot * NCT + c) * 64 + lane] = rs[c].l;
-        }
-    };
-    auto add = [&](int slot) {
-#pragma unroll
-        for (int c = 0; c < NCT; ++c) {
-#pragma unroll
-            for (int mt = 0; mt < D / 32; ++mt)
-#pragma unroll
-                for (int i = 0; i < 16; ++i)
-                    rs[c].o[mt][i] += obuf[((slot * NCT + c) * 64 + mt * 16 + i) * 64 + lane];
-            rs[c].l += lbuf[(slot * NCT + c) * 64 + lane];
-        }
-    };
-    if (wave >= 2) put(wave - 2);     // round 1: waves 2, 3 -> slots 0, 1
+            for (int q4 = 0; q4 < 4; ++q4)
+                obuf[((slot * NCT + c) * 4 + q4) * 64 + lane] =
+                    make_float4(rs[c].o[mt][4 * q4], rs[c].o[mt][4 * q4 + 1], rs[c].o[mt][4 * q4 + 2],
+                                rs[c].o[mt][4 * q4 + 3]);
+    }
     __syncthreads();
-    if (wave < 2) add(wave);          // wave 0 += wave 2, wave 1 += wave 3
-    __syncthreads();
-    if (wave == 1) put(0);            // round 2: wave 1 -> slot 0
-    __syncthreads();
-    if (wave != 0) return;
-    add(0);                           // wave 0 holds the workgroup's result
-
-    Work w{};
-    w.g = g;
-    w.split = split;
-    w.tok0 = 0;
-#pragma unroll
-    for (int c = 0; c < NCT; ++c) epilogue<D, kModeContinue>(p, w, rs[c], 32 * c + j, valid[c], tok[c], head[c], grp);
+    switch (wave) {
+        case 0: finish_quarter<NCT, 0>(p, rs, obuf, lbuf, mbuf, valid, tok, head, g, split, lane); break;
+        case 1: finish_quarter<NCT, 1>(p, rs, obuf, lbuf, mbuf, valid, tok, head, g, split, lane); break;
+        case 2: finish_quarter<NCT, 2>(p, rs, obuf, lbuf, mbuf, valid, tok, head, g, split, lane); break;
+        default: finish_quarter<NCT, 3>(p, rs, obuf, lbuf, mbuf, valid, tok, head, g, split, lane); break;
+    }
 }
 
 }  // namespace

@@ -1,0 +1,104 @@
+// merge.hip -- combine the per-split partial results of a split continuation
+// (fixed split order, so the result is reproducible bit for bit):
+//   M = max_s m_s,  w_s = 2^(m_s - M),  out = sum_s w_s O_s / sum_s w_s l_s
+// which is the log-sum-exp merge of partial softmax sums.
+//
+// One lane per 4 consecutive head-dim values of one row: a 256-lane
+// workgroup covers 256 / (D/4) rows of one kv head (8 at D = 128, 16 at
+// D = 64).  The lanes of a row first build the split weights together --
+// lane k takes splits k, k + D/4, ...; the row maximum and l come from xor
+// butterflies inside the row's lanes (same bits in every lane); the weights
+// go through LDS -- then every lane streams its 16 bytes of every split with
+// 16 loads in flight.  Block b serves kv head b % Hkv, the same residue the
+// attention kernel gives the head's blocks, so with 8 kv heads the partials
+// are read on the XCD whose L2 took them.
+#include "attn_common.hpp"
+
+namespace kvr {
+namespace {
+
+using namespace dev;
+
+constexpr int MERGE_THREADS = 256;
+constexpr int MERGE_BATCH = 16;   // split loads in flight per lane
+
+template <int D>
+__global__ __launch_bounds__(MERGE_THREADS) void merge_bf16_kernel(const MergeParams p) {
+    constexpr int CPR = D / 4;                 // lanes per row
+    constexpr int RPW = MERGE_THREADS / CPR;   // rows per workgroup
+    __shared__ float wts[RPW][kMaxSplits + 1];
+    const int tid = threadIdx.x;
+    const int rr = tid / CPR;
+    const int part = tid % CPR;
+    const int g = blockIdx.x % p.n_kv_heads;
+    const int r0 = (blockIdx.x / p.n_kv_heads) * RPW;
+    const int r = r0 + rr;
+    const bool valid = r < p.rows;
+    const int64_t per_split = (int64_t)p.n_kv_heads * p.rows;
+    const float *ml = p.ws + (int64_t)p.nsplit * per_split * D;
+    const int64_t row = (int64_t)g * p.rows + (valid ? r : r0);   // rows past the end read row r0
+
+    float M = -INFINITY;
+    for (int s = part; s < p.nsplit; s += CPR) M = fmaxf(M, ml[(s * per_split + row) * 2]);
+#pragma unroll
+    for (int x = 1; x < CPR; x <<= 1) M = fmaxf(M, __shfl_xor(M, x));
+    float l = 0.f;
+    for (int s = part; s < p.nsplit; s += CPR) {
+        const float2 v = *(const float2 *)(ml + (s * per_split + row) * 2);
+        const float w = __builtin_amdgcn_exp2f(v.x - M);
+        wts[rr][s] = w;
+        l = __builtin_fmaf(w, v.y, l);
+    }
+#pragma unroll
+    for (int x = 1; x < CPR; x <<= 1) l += __shfl_xor(l, x);
+    __syncthreads();
+    if (!valid) return;
+
+    const float *src = p.ws + row * D + 4 * part;
+    const int64_t sstride = per_split * D;
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+    int s = 0;
+    for (; s + MERGE_BATCH <= p.nsplit; s += MERGE_BATCH) {
+        float4 o[MERGE_BATCH];
+#pragma unroll
+        for (int k = 0; k < MERGE_BATCH; ++k) o[k] = *(const float4 *)(src + (s + k) * sstride);
+#pragma unroll
+        for (int k = 0; k < MERGE_BATCH; ++k) {
+            const float w = wts[rr][s + k];
+            acc.x = __builtin_fmaf(w, o[k].x, acc.x);
+            acc.y = __builtin_fmaf(w, o[k].y, acc.y);
+            acc.z = __builtin_fmaf(w, o[k].z, acc.z);
+            acc.w = __builtin_fmaf(w, o[k].w, acc.w);
+        }
+    }
+    for (; s < p.nsplit; ++s) {
+        const float4 o = *(const float4 *)(src + s * sstride);
+        const float w = wts[rr][s];
+        acc.x = __builtin_fmaf(w, o.x, acc.x);
+        acc.y = __builtin_fmaf(w, o.y, acc.y);
+        acc.z = __builtin_fmaf(w, o.z, acc.z);
+        acc.w = __builtin_fmaf(w, o.w, acc.w);
+    }
+    const float il = l > 0.f ? 1.f / l : 0.f;
+    const int tok = r / p.group;
+    const int head = g * p.group + r % p.group;
+    __bf16 *out = (__bf16 *)p.out + ((int64_t)tok * p.n_q_heads + head) * D + 4 * part;
+    u32x2 v;
+    v[0] = pack_bf16x2(acc.x * il, acc.y * il);
+    v[1] = pack_bf16x2(acc.z * il, acc.w * il);
+    *(u32x2 *)out = v;
+}
+
+}  // namespace
+
+hipError_t launch_merge_bf16(const MergeParams &p, int head_dim, hipStream_t s) {
+    const int rpw = MERGE_THREADS / (head_dim / 4);
+    const int grid = (p.rows + rpw - 1) / rpw * p.n_kv_heads;
+    if (head_dim == 128)
+        hipLaunchKernelGGL(merge_bf16_kernel<128>, dim3(grid), dim3(MERGE_THREADS), 0, s, p);
+    else
+        hipLaunchKernelGGL(merge_bf16_kernel<64>, dim3(grid), dim3(MERGE_THREADS), 0, s, p);
+    return hipGetLastError();
+}
+
+}  // namespace kvr
