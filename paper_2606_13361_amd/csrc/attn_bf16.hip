@@ -93,10 +93,14 @@ void attn_bf16_kernel(const AttnParams p) {
     // the end of the range or holding this workgroup's own prefill tokens take
     // the general path, where rows past ke are clamped to a valid row (they lie
     // beyond every row's causal bound, so they are masked and never count).
-    const uint32_t cache_off = (uint32_t)(srow * D * 2 + 16 * sc);
-    const uint32_t new_off = (uint32_t)(srow * nstride * 2 + 16 * sc);
-    const uint32_t cache_pass = (uint32_t)(T::RPP * D * 2);
-    const uint32_t new_pass = (uint32_t)(T::RPP * nstride * 2);
+    // 32-bit byte offsets per pass: interior tiles load through a buffer
+    // resource (uniform base in SGPRs) plus these per-lane offsets
+    uint32_t coff[T::KPT], noff[T::KPT];
+#pragma unroll
+    for (int i = 0; i < T::KPT; ++i) {
+        coff[i] = (uint32_t)((srow + T::RPP * i) * D * 2 + 16 * sc);
+        noff[i] = (uint32_t)((srow + T::RPP * i) * nstride * 2 + 16 * sc);
+    }
     const int64_t cache_end = ke < npre ? ke : npre;   // keys [.., cache_end) come from the cache
     int64_t own_lo = 0, own_hi = -1;                   // prefill tokens whose cache row this WG stores
     if constexpr (MODE == kModePrefill) {
@@ -110,18 +114,18 @@ void attn_bf16_kernel(const AttnParams p) {
     auto gload = [&](int64_t k0) {
         const bool own = MODE == kModePrefill && k0 <= own_hi && k0 + BN > own_lo;
         if (k0 + BN <= cache_end) {
-            const unsigned char *kb_ = kc0 + k0 * D * 2, *vb_ = vc0 + k0 * D * 2;
+            const auto rk = buf_rsrc(kc0 + k0 * D * 2), rv = buf_rsrc(vc0 + k0 * D * 2);
 #pragma unroll
             for (int i = 0; i < T::KPT; ++i) {
-                kreg[i] = *(const u32x4 *)(kb_ + cache_off + i * cache_pass);
-                vreg[i] = *(const u32x4 *)(vb_ + cache_off + i * cache_pass);
+                kreg[i] = buf_load16(rk, coff[i]);
+                vreg[i] = buf_load16(rv, coff[i]);
             }
         } else if (k0 >= npre && k0 + BN <= ke && !own) {
-            const unsigned char *kb_ = kn0 + (k0 - npre) * nstride * 2, *vb_ = vn0 + (k0 - npre) * nstride * 2;
+            const auto rk = buf_rsrc(kn0 + (k0 - npre) * nstride * 2), rv = buf_rsrc(vn0 + (k0 - npre) * nstride * 2);
 #pragma unroll
             for (int i = 0; i < T::KPT; ++i) {
-                kreg[i] = *(const u32x4 *)(kb_ + new_off + i * new_pass);
-                vreg[i] = *(const u32x4 *)(vb_ + new_off + i * new_pass);
+                kreg[i] = buf_load16(rk, noff[i]);
+                vreg[i] = buf_load16(rv, noff[i]);
             }
         } else {
 #pragma unroll

@@ -138,6 +138,24 @@ __device__ __forceinline__ void dma16(const void *src, const void *lds_dst) {
     const uint32_t lds = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void *)lds_dst;
     asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(lds), "v"(src) : "m0");
 }
+// The same with a wave-uniform 64-bit base in SGPRs and a 32-bit per-lane
+// byte offset (the instruction's saddr form): no per-lane address arithmetic.
+__device__ __forceinline__ void dma16_s(uint64_t base, uint32_t off, const void *lds_dst) {
+    const uint32_t lds = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void *)lds_dst;
+    asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2" ::"s"(lds), "v"(off), "s"(base) : "m0");
+}
+
+// 16-byte load through a buffer resource: the 64-bit base lives in SGPRs
+// (one per tile, built with scalar arithmetic) and each lane supplies a
+// 32-bit byte offset, so interior tiles need no per-lane address arithmetic.
+// Raw buffer, stride 0, range 2^31 - 1 bytes (every offset used is far
+// below); dword 3 = 0x00020000 is the gfx9-family format word (32-bit data).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buf_rsrc(const void *base) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), 0, 0x7fffffff, 0x00020000);
+}
+__device__ __forceinline__ u32x4 buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+    return __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 0);
+}
 
 // s_waitcnt with vmcnt = N and the other counters left alone (gfx9 encoding:
 // vmcnt[3:0] bits 3:0, expcnt bits 6:4, lgkmcnt bits 11:8, vmcnt[5:4] bits 15:14).

@@ -188,9 +188,9 @@ __global__ __launch_bounds__(THREADS) void attn_cont_kernel(const AttnParams p) 
         if (key0 + SKEYS <= cache_end) {
             const uint64_t kb_ = kc_a + (uint64_t)key0 * ROWB, vb_ = vc_a + (uint64_t)key0 * ROWB;
 #pragma unroll
-            for (int i = 0; i < 8; ++i) dma16((const void *)(kb_ + off_c[i]), kd + 1024 * i);
+            for (int i = 0; i < 8; ++i) dma16_s(kb_, off_c[i], kd + 1024 * i);
 #pragma unroll
-            for (int i = 0; i < 8; ++i) dma16((const void *)(vb_ + off_c[i]), vd + 1024 * i);
+            for (int i = 0; i < 8; ++i) dma16_s(vb_, off_c[i], vd + 1024 * i);
         } else {
             // prefix/new boundary, new rows or a ragged end: per-row source;
             // rows past ke clamp to a valid row (beyond every causal bound, masked)

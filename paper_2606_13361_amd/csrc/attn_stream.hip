@@ -1,6 +1,5 @@
 // attn_stream.hip -- the streamed member of the bf16 attention family, for
-// the modes that read a long cached prefix: continue (HBM-bound) and many
-// readers, head_dim 128.
+// many readers of one long cached prefix, head_dim 128.
 //
 // K/V tiles go from global memory straight into LDS (global_load_lds_dwordx4,
 // no registers on the way), NSTAGE tiles deep: NSTAGE-1 tiles are in flight
@@ -105,16 +104,16 @@ __device__ __forceinline__ void stream_body(const AttnParams &p) {
         if (k0 + KEYS <= cache_end) {                     // all rows cached
             const uint64_t kb_ = kc_a + (uint64_t)k0 * ROW_BYTES, vb_ = vc_a + (uint64_t)k0 * ROW_BYTES;
 #pragma unroll
-            for (int i = 0; i < NL; ++i) dma16((const void *)(kb_ + off_c[i]), kd + 1024 * i);
+            for (int i = 0; i < NL; ++i) dma16_s(kb_, off_c[i], kd + 1024 * i);
 #pragma unroll
-            for (int i = 0; i < NL; ++i) dma16((const void *)(vb_ + off_c[i]), vd + 1024 * i);
+            for (int i = 0; i < NL; ++i) dma16_s(vb_, off_c[i], vd + 1024 * i);
         } else if (k0 >= npre && k0 + KEYS <= ke) {       // all rows new
             const uint64_t kb_ = kn_a + (uint64_t)(k0 - npre) * (uint64_t)nstride_b;
             const uint64_t vb_ = vn_a + (uint64_t)(k0 - npre) * (uint64_t)nstride_b;
 #pragma unroll
-            for (int i = 0; i < NL; ++i) dma16((const void *)(kb_ + off_n[i]), kd + 1024 * i);
+            for (int i = 0; i < NL; ++i) dma16_s(kb_, off_n[i], kd + 1024 * i);
 #pragma unroll
-            for (int i = 0; i < NL; ++i) dma16((const void *)(vb_ + off_n[i]), vd + 1024 * i);
+            for (int i = 0; i < NL; ++i) dma16_s(vb_, off_n[i], vd + 1024 * i);
         } else {
             // mixed or ragged stage: rows past ke clamp to a valid row (beyond every
             // row's causal bound, masked, never counted)
@@ -124,8 +123,13 @@ __device__ __forceinline__ void stream_body(const AttnParams &p) {
                 const int64_t kk = key < ke ? key : ke - 1;
                 const bool in_cache = kk < npre;
                 const uint64_t off = in_cache ? (uint64_t)kk * ROW_BYTES : (uint64_t)(kk - npre) * (uint64_t)nstride_b;
-                dma16((const void *)((in_cache ? kc_a : kn_a) + off + lchunk[i]), kd + 1024 * i);
-                dma16((const void *)((in_cache ? vc_a : vn_a) + off + lchunk[i]), vd + 1024 * i);
+                // base select by mask (a plain select of the two uniform bases was
+                // lowered through private memory)
+                const uint64_t sel = 0 - (uint64_t)in_cache;
+                const uint64_t kbase = (kc_a & sel) | (kn_a & ~sel);
+                const uint64_t vbase = (vc_a & sel) | (vn_a & ~sel);
+                dma16((const void *)(kbase + off + lchunk[i]), kd + 1024 * i);
+                dma16((const void *)(vbase + off + lchunk[i]), vd + 1024 * i);
             }
         }
     };
@@ -188,12 +192,6 @@ __device__ __forceinline__ void stream_body(const AttnParams &p) {
     epilogue<D, MODE>(p, w, rs, r, valid, tok, head, grp);
 }
 
-// continue: 4 stages of 32 keys (64 KB of LDS): two workgroups per CU, each with
-// 3 stages in flight
-__global__ __launch_bounds__(THREADS) __attribute__((amdgpu_waves_per_eu(2, 2)))
-void attn_stream_continue_kernel(const AttnParams p) {
-    stream_body<kStreamStagesContinue, kStreamSubContinue, kModeContinue>(p);
-}
 // many readers: two workgroups per CU, so registers must fit two waves per SIMD
 __global__ __launch_bounds__(THREADS) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void attn_stream_readers_kernel(const AttnParams p) {
@@ -202,11 +200,8 @@ void attn_stream_readers_kernel(const AttnParams p) {
 
 }  // namespace
 
-hipError_t launch_attn_stream(const AttnParams &p, int mode, int grid, hipStream_t s) {
-    if (mode == kModeContinue)
-        hipLaunchKernelGGL(attn_stream_continue_kernel, dim3(grid), dim3(THREADS), 0, s, p);
-    else
-        hipLaunchKernelGGL(attn_stream_readers_kernel, dim3(grid), dim3(THREADS), 0, s, p);
+hipError_t launch_attn_stream_readers(const AttnParams &p, int grid, hipStream_t s) {
+    hipLaunchKernelGGL(attn_stream_readers_kernel, dim3(grid), dim3(THREADS), 0, s, p);
     return hipGetLastError();
 }
 

@@ -282,7 +282,7 @@ int kvr_continue_batched(const kvr_desc *desc, const void *Qs, const void *Ks, c
         p.tiles_total = tiles;
         p.rows_total = 0;
         const int64_t grid = (int64_t)tiles * p.n_kv_heads;
-        hipError_t e = use_stream(desc) ? launch_attn_stream(p, kModeReaders, (int)grid, (hipStream_t)stream)
+        hipError_t e = use_stream(desc) ? launch_attn_stream_readers(p, (int)grid, (hipStream_t)stream)
                        : desc->dtype == KVR_BF16 ? launch_attn_bf16(p, desc->head_dim, kModeReaders, (int)grid,
                                                                     (hipStream_t)stream)
                                                : launch_attn_f32(p, desc->head_dim, (int)grid, (hipStream_t)stream);
