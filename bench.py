@@ -201,17 +201,29 @@ def main():
         "claim1_maxabs": claim1,
         "paper_context": "paper Table 1: full-model reuse 8.6-49.7x cheaper (Qwen3-4B fp16, Apple M1 Pro "
                          "MPS, one continuation step); not comparable hardware or scope",
-        "roofline": {
-            "kernel": "attn_bf16_kernel<128, prefill>",
-            "bound": "mfma",
-            "achieved": round(pf_tflops, 2),
-            "peak": PEAK_BF16_TFLOPS,
-            "unit": "TFLOP/s",
-            "frac": round(pf_tflops / PEAK_BF16_TFLOPS, 4),
-            "traffic": None,
-            "flops_per_launch": pf_flops,
-        },
     }
+    # rooflines of the step's kernels; `roofline` is the one that takes the most time
+    digest = kernel_source_digest()
+    traffic = measured_traffic(digest)
+    roofs = {
+        "readers": {"kernel": "attn_stream_readers_kernel", "bound": "mfma", "achieved": round(rd_tflops, 2),
+                    "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(rd_tflops / PEAK_BF16_TFLOPS, 4),
+                    "work_per_launch": rd_flops, "avg_launch_ms": round(avg["readers"] * 1e3, 4)},
+        "prefill": {"kernel": "attn_bf16_kernel<128, prefill>", "bound": "mfma", "achieved": round(pf_tflops, 2),
+                    "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(pf_tflops / PEAK_BF16_TFLOPS, 4),
+                    "work_per_launch": pf_flops, "avg_launch_ms": round(avg["prefill"] * 1e3, 4)},
+        "continue": {"kernel": "attn_cont_kernel<3> + merge_bf16_kernel<128>", "bound": "hbm",
+                     "achieved": round(c_gbps, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
+                     "frac": round(c_gbps / PEAK_HBM_GBPS, 4), "work_per_launch": c_bytes,
+                     "avg_launch_ms": round(avg["continue"] * 1e3, 4)},
+    }
+    for r in roofs.values():
+        t = traffic.get(r["kernel"])
+        r["traffic"] = t
+    dominant = max(roofs, key=lambda k: roofs[k]["avg_launch_ms"])
+    result["roofline"] = dict(roofs[dominant], call=dominant)
+    result["rooflines"] = roofs
+    result["kernel_source_digest"] = digest
 
     if not args.no_sweep:
         lens_ = [int(x) for x in args.sweep_lengths.split(",")] if args.sweep_lengths else list(W.SWEEP_L)
@@ -221,6 +233,39 @@ def main():
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(q, k, v, A, args.cpu_seconds)
     print(json.dumps(result), flush=True)
+
+
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_per_launch.md")
+
+
+def kernel_source_digest():
+    """Digest of every kernel source file: counter figures taken for other sources are stale."""
+    import hashlib
+    csrc = os.path.join(ROOT, "paper_2606_13361_amd", "csrc")
+    h = hashlib.sha256()
+    for fn in sorted(os.listdir(csrc)):
+        if fn.endswith((".hip", ".hpp")):
+            h.update(fn.encode())
+            with open(os.path.join(csrc, fn), "rb") as f:
+                h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(digest):
+    """HBM bytes per launch (FETCH + WRITE, calibrated) from the committed rocprofv3
+    summary, keyed by kernel; empty when that summary was taken for other sources."""
+    try:
+        lines = open(TRAFFIC_FILE).read().splitlines()
+    except OSError:
+        return {}
+    if not any(ln.strip() == "source digest: " + digest for ln in lines):
+        return {}
+    out = {}
+    for ln in lines:
+        cells = [c.strip() for c in ln.strip().strip("|").split("|")]
+        if len(cells) >= 5 and cells[0].startswith("`") and cells[-1].replace(".", "").isdigit():
+            out[cells[0].strip("`")] = int(float(cells[-1]))
+    return out
 
 
 def graph_time(torch, stream, issue, n_calls, replays=5):

@@ -180,14 +180,23 @@ __device__ __forceinline__ void tile_step(RowState<D> &rs, const u32x4 (&qf)[D /
                                           bool mask, int lim, float c2, int grp) {
     f32x16 s[NSUB];
 #pragma unroll
-    for (int st = 0; st < NSUB; ++st) {
+    for (int st = 0; st < NSUB; ++st)
 #pragma unroll
         for (int i = 0; i < 16; ++i) s[st][i] = 0.f;
+    // K fragments one head-dim step ahead of the MFMAs that consume them, the
+    // NSUB accumulation chains interleaved
+    u32x4 a[2][NSUB];
 #pragma unroll
-        for (int ks = 0; ks < D / 16; ++ks) {
-            const u32x4 a = *(const u32x4 *)kaddr(st, ks);
-            s[st] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a), as_bf16x8(qf[ks]), s[st], 0, 0, 0);
+    for (int st = 0; st < NSUB; ++st) a[0][st] = *(const u32x4 *)kaddr(st, 0);
+#pragma unroll
+    for (int ks = 0; ks < D / 16; ++ks) {
+        if (ks + 1 < D / 16) {
+#pragma unroll
+            for (int st = 0; st < NSUB; ++st) a[(ks + 1) & 1][st] = *(const u32x4 *)kaddr(st, ks + 1);
         }
+#pragma unroll
+        for (int st = 0; st < NSUB; ++st)
+            s[st] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a[ks & 1][st]), as_bf16x8(qf[ks]), s[st], 0, 0, 0);
     }
     // causal mask: tile key offset 32*st + 8*(i/4) + 4*grp + i%4 is visible iff <= lim
     if (mask) {
