@@ -1,0 +1,353 @@
+// attn_pp.hip -- prefill, bf16, head_dim 128: the two-group ("ping-pong")
+// member of the attention family.
+//
+// A workgroup is 8 waves, 2 per SIMD, holding 256 query rows of one kv head
+// (32 rows per wave, GQA-packed as everywhere in the family).  Waves 0-3 form
+// group A, waves 4-7 group B; the two waves sharing a SIMD belong to
+// different groups.  Per 64-key tile t a group runs two steps:
+//   GEMM(t)  O += V_{t-1} P_{t-1}  and  S_t = K_t Q^T     (32 MFMAs)
+//   SOFT(t)  mask, row max, lazy rescale, P_t = exp2(...) (VALU)
+// and the groups are offset by one step: while A runs GEMM(t), B runs
+// SOFT(t-1); while A runs SOFT(t), B runs GEMM(t).  Every step ends at a
+// workgroup barrier, so each SIMD always has one wave feeding the matrix core
+// and one wave on the vector ALU.  The wave in its GEMM step runs at raised
+// wave priority (s_setprio), so its MFMAs are not starved by the other
+// wave's vector stream; without it the older wave slot wins and the phases
+// where the younger wave multiplies run about 40 % longer.
+//
+// K/V tiles reach LDS by direct loads (global_load_lds_dwordx4) into a ring
+// of 4 stages of 32 KB: tile t is issued four steps before its first use and
+// its stage is refilled only after both groups have read it.  Rows are
+// unpadded 256-byte rows with the 16-byte chunk c of row r in slot
+// c ^ swz(r) (conflict-free K reads and transposing V reads).
+//
+// The workgroup holding the first query row of a token also copies that
+// token's K/V rows into the cache, after its attention work.
+#include "attn_common.hpp"
+
+namespace kvr {
+namespace {
+
+using namespace dev;
+
+constexpr int D = 128;
+constexpr int ROWB = D * 2;               // 256 bytes per K/V row
+constexpr int KEYS = 64;                  // keys per tile
+constexpr int TILE = KEYS * ROWB;         // 16 KB: K (or V) of one tile
+constexpr int STAGE = 2 * TILE;           // 32 KB
+constexpr int NS = 4;                     // ring stages: 128 KB of LDS
+constexpr int PP_THREADS = 512;
+constexpr int PP_LOADS = 4;               // direct loads per wave per tile (2 K + 2 V)
+
+__device__ __forceinline__ int swz(int row) { return ((row >> 2) & 3) | ((row & 3) << 2); }
+
+__global__ __launch_bounds__(PP_THREADS) void attn_pp_kernel(const AttnParams p) {
+    __shared__ __attribute__((aligned(1024))) unsigned char smem[NS * STAGE];
+
+    const int tid = threadIdx.x;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform: scalar branches
+    const int gw = wave >> 2;                                    // group: 0 = A, 1 = B
+    const int lane = tid & 63;
+    const int j = lane & 31;
+    const int grp = lane >> 5;
+
+    // ---- work: kv head fastest (XCD locality), row tiles longest first
+    const int G = p.group;
+    const int g = blockIdx.x % p.n_kv_heads;
+    const int tile = p.tiles_total - 1 - blockIdx.x / p.n_kv_heads;
+    const int L = p.seg_tok0[1];
+    const int R = G * L;
+    const int row0 = tile * kRowsPP;
+    const int row_last = min(row0 + kRowsPP, R) - 1;
+    const int ke = row_last / G + 1;                              // keys any row here may see
+    const int ntiles = (ke + KEYS - 1) / KEYS;
+
+    const int r = row0 + wave * 32 + j;
+    const bool valid = r < R;
+    const int tok = valid ? r / G : 0;
+    const int head = g * G + (valid ? r % G : 0);
+    const int pos = valid ? tok : -1;
+    const int wrow0 = row0 + wave * 32;
+    const bool wave_active = wrow0 < R;
+    const int k_full = wave_active ? wrow0 / G + 1 : 0;          // keys every row of this wave sees
+
+    u32x4 qf[D / 16];
+    {
+        const __bf16 *qrow = (const __bf16 *)p.q + ((int64_t)tok * p.n_q_heads + head) * D;
+#pragma unroll
+        for (int ks = 0; ks < D / 16; ++ks)
+            qf[ks] = valid ? *(const u32x4 *)(qrow + 16 * ks + 8 * grp) : (u32x4){0, 0, 0, 0};
+    }
+
+    // ---- load map: wave w moves K rows 8w..8w+7 and V rows 8w..8w+7 of a tile,
+    // 4 rows per instruction; lane -> row 8w + 4i + lane/16, LDS slot lane%16,
+    // global chunk slot ^ swz(row)
+    const int64_t nstride_b = (int64_t)p.n_kv_heads * ROWB;
+    const uint64_t kn_a = (uint64_t)(uintptr_t)p.kn + (uint64_t)g * ROWB;
+    const uint64_t vn_a = (uint64_t)(uintptr_t)p.vn + (uint64_t)g * ROWB;
+    int lrow[2];
+    uint32_t lchunk[2], off_n[2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        lrow[i] = 8 * wave + 4 * i + (lane >> 4);
+        lchunk[i] = 16u * (uint32_t)((lane & 15) ^ swz(lrow[i]));
+        off_n[i] = (uint32_t)(lrow[i] * nstride_b) + lchunk[i];
+    }
+    auto load_tile = [=](int t) {
+        const int k0 = t * KEYS;
+        const unsigned char *kd = smem + (t % NS) * STAGE + 8 * wave * ROWB;
+        const unsigned char *vd = kd + TILE;
+        if (k0 + KEYS <= ke) {
+            const uint64_t kb_ = kn_a + (uint64_t)k0 * nstride_b, vb_ = vn_a + (uint64_t)k0 * nstride_b;
+#pragma unroll
+            for (int i = 0; i < 2; ++i) dma16_s(kb_, off_n[i], kd + 1024 * i);
+#pragma unroll
+            for (int i = 0; i < 2; ++i) dma16_s(vb_, off_n[i], vd + 1024 * i);
+        } else {
+            // ragged last tile: rows past ke repeat row ke-1 (beyond every causal bound, masked)
+#pragma unroll
+            for (int i = 0; i < 2; ++i) {
+                const int key = min(k0 + lrow[i], ke - 1);
+                const uint64_t off = (uint64_t)key * (uint64_t)nstride_b + lchunk[i];
+                dma16((const void *)(kn_a + off), kd + 1024 * i);
+                dma16((const void *)(vn_a + off), vd + 1024 * i);
+            }
+        }
+    };
+
+    // ---- read maps (per lane, loop invariant); as in the streamed kernel
+    uint32_t ka[D / 16];
+#pragma unroll
+    for (int ks = 0; ks < D / 16; ++ks) ka[ks] = (uint32_t)j * ROWB + 16u * (uint32_t)((2 * ks + grp) ^ swz(j));
+    const int l16 = lane & 15;
+    const int g16 = lane >> 4;
+    uint32_t va[2][D / 32];
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int mt = 0; mt < D / 32; ++mt) {
+            const int row = 8 * h + 4 * (g16 >> 1) + (l16 >> 2);
+            const int chunk = (32 * mt + 16 * (g16 & 1) + 4 * (l16 & 3)) / 8;
+            va[h][mt] = (uint32_t)row * ROWB + 16u * (uint32_t)(chunk ^ swz(row)) + 8u * (uint32_t)(l16 & 1);
+        }
+
+    RowState<D> rs;
+    rs.zero();
+    const float c2 = p.scale_log2;
+    f32x16 s[2];            // S_t^T of the two 32-key sub-tiles (GEMM(t) -> SOFT(t))
+    u32x4 pf[2][2];         // P_t^T as bf16 (SOFT(t) -> GEMM(t+1))
+#pragma unroll
+    for (int st = 0; st < 2; ++st) {
+#pragma unroll
+        for (int i = 0; i < 16; ++i) s[st][i] = 0.f;
+        pf[st][0] = pf[st][1] = (u32x4){0, 0, 0, 0};
+    }
+
+    // GEMM(t): O += V_{t-1} P_{t-1} (t >= 1), S_t = K_t Q^T (t < ntiles), as 8
+    // chunks of 2 S and 2 PV MFMAs; chunk c+1's LDS fragments are read while
+    // chunk c's MFMAs run, and nothing moves across chunks (bounded registers)
+    auto kfrag = [&](const unsigned char *ks_, int st, int ks) {
+        return *(const u32x4 *)(ks_ + ka[ks] + 32 * st * ROWB);
+    };
+    auto vfrag = [&](const unsigned char *vs_, int idx) {   // PV product idx = (st, kk, mt)
+        const int st = idx >> 3, kk = (idx >> 2) & 1, mt = idx & 3;
+        const unsigned char *b = vs_ + (32 * st + 16 * kk) * ROWB;
+        const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)(b + va[0][mt]));
+        const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)(b + va[1][mt]));
+        const u32x2 lo2 = __builtin_bit_cast(u32x2, lo);
+        const u32x2 hi2 = __builtin_bit_cast(u32x2, hi);
+        return (u32x4){lo2[0], lo2[1], hi2[0], hi2[1]};
+    };
+    auto pv = [&](const u32x4 &a, int idx) {
+        const int st = idx >> 3, kk = (idx >> 2) & 1, mt = idx & 3;
+        rs.o[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a), as_bf16x8(pf[st][kk]), rs.o[mt], 0, 0, 0);
+    };
+    auto sm = [&](const u32x4 &a, int st, int ks) {
+        s[st] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a), as_bf16x8(qf[ks]), s[st], 0, 0, 0);
+    };
+    auto s_zero = [&]() {
+#pragma unroll
+        for (int st = 0; st < 2; ++st)
+#pragma unroll
+            for (int i = 0; i < 16; ++i) s[st][i] = 0.f;
+    };
+    auto gemm_s = [&](int t) {            // S only (first tile)
+        const unsigned char *ks_ = smem + (t % NS) * STAGE;
+        s_zero();
+#pragma unroll
+        for (int ks = 0; ks < D / 16; ++ks)
+#pragma unroll
+            for (int st = 0; st < 2; ++st) sm(kfrag(ks_, st, ks), st, ks);
+    };
+    auto gemm_pv = [&](int t) {           // PV only (after the last tile)
+        const unsigned char *vs_ = smem + ((t + NS - 1) % NS) * STAGE + TILE;
+#pragma unroll
+        for (int idx = 0; idx < 16; ++idx) pv(vfrag(vs_, idx), idx);
+    };
+    auto gemm = [&](int t) {              // both
+        const unsigned char *ks_ = smem + (t % NS) * STAGE;
+        const unsigned char *vs_ = smem + ((t + NS - 1) % NS) * STAGE + TILE;
+        s_zero();
+        u32x4 k0 = kfrag(ks_, 0, 0), k1 = kfrag(ks_, 1, 0), v0 = vfrag(vs_, 0), v1 = vfrag(vs_, 1);
+#pragma unroll
+        for (int c = 0; c < 8; ++c) {
+            u32x4 nk0, nk1, nv0, nv1;
+            if (c + 1 < 8) {
+                nk0 = kfrag(ks_, 0, c + 1);
+                nk1 = kfrag(ks_, 1, c + 1);
+                nv0 = vfrag(vs_, 2 * c + 2);
+                nv1 = vfrag(vs_, 2 * c + 3);
+            }
+            sm(k0, 0, c);
+            pv(v0, 2 * c);
+            sm(k1, 1, c);
+            pv(v1, 2 * c + 1);
+            __builtin_amdgcn_sched_barrier(0);
+            if (c + 1 < 8) {
+                k0 = nk0; k1 = nk1; v0 = nv0; v1 = nv1;
+            }
+        }
+    };
+    // SOFT(t): causal mask, row max, lazy rescale of (O, l), P_t = 2^(S c2 - m)
+    auto soft = [&](int t) {
+        const int k0 = t * KEYS;
+        if (k0 + KEYS > k_full) {
+            const int lim = max(-1, min(pos - k0, KEYS));
+#pragma unroll
+            for (int st = 0; st < 2; ++st)
+#pragma unroll
+                for (int i = 0; i < 16; ++i) {
+                    const int o = 32 * st + 8 * (i >> 2) + 4 * grp + (i & 3);
+                    if (o > lim) s[st][i] = -INFINITY;
+                }
+        }
+        // row max as a tree (5 dependent levels instead of a 32-long chain)
+        float v[32];
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+            v[i] = s[0][i];
+            v[16 + i] = s[1][i];
+        }
+#pragma unroll
+        for (int w = 16; w >= 1; w >>= 1)
+#pragma unroll
+            for (int i = 0; i < w; ++i) v[i] = fmaxf(v[i], v[i + w]);
+        const float mx = pair_max(v[0]) * c2;
+        const bool need = mx > rs.m + kRescaleSlack;
+        if (__ballot(need)) {
+            const float m_new = need ? mx : rs.m;
+            const float alpha = __builtin_amdgcn_exp2f(rs.m - m_new);
+            rs.m = m_new;
+            rs.l *= alpha;
+#pragma unroll
+            for (int mt = 0; mt < D / 32; ++mt)
+#pragma unroll
+                for (int i = 0; i < 16; ++i) rs.o[mt][i] *= alpha;
+        }
+        // four independent partial sums of the bf16 weights
+        float lsum[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int st = 0; st < 2; ++st)
+#pragma unroll
+            for (int i = 0; i < 16; i += 2) {
+                const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[st][i], c2, -rs.m));
+                const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[st][i + 1], c2, -rs.m));
+                const uint32_t pk = pack_bf16x2(p0, p1);
+                float &acc = lsum[(i >> 1) & 3];
+                acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, pk), kOnes, acc, false);
+                pf[st][i >> 3][(i & 7) >> 1] = pk;
+            }
+        rs.l += (lsum[0] + lsum[1]) + (lsum[2] + lsum[3]);
+    };
+
+    // ---- steps.  Phase 2t starts once tile t has landed (each wave waits for its
+    // own loads, then the barrier) and issues tile t+2, whose stage held tile t-2
+    // and was last read in phase 2t-1.  Group A: GEMM(t) in phase 2t, SOFT(t)
+    // in phase 2t+1; group B one phase later.  Both run 2*ntiles + 2 phases.
+    auto sync = [&](int phi) {
+        __builtin_amdgcn_sched_barrier(0);
+        if ((phi & 1) == 0) {
+            const int t = phi >> 1;
+            if (t + 1 < ntiles) wait_vmcnt<PP_LOADS>();   // tile t landed, tile t+1 may still fly
+            else wait_vmcnt<0>();
+            __builtin_amdgcn_s_barrier();
+            asm volatile("" ::: "memory");
+            if (t + 2 < ntiles) load_tile(t + 2);
+        } else {
+            __builtin_amdgcn_s_barrier();
+            asm volatile("" ::: "memory");
+        }
+        __builtin_amdgcn_sched_barrier(0);
+    };
+    load_tile(0);
+    if (ntiles > 1) load_tile(1);
+    const bool act = wave_active;
+    if (gw == 0) {
+        sync(0);
+        if (act) { __builtin_amdgcn_s_setprio(1); gemm_s(0); __builtin_amdgcn_s_setprio(0); }
+        sync(1);
+        if (act) soft(0);
+        for (int t = 1; t < ntiles; ++t) {
+            sync(2 * t);
+            if (act) { __builtin_amdgcn_s_setprio(1); gemm(t); __builtin_amdgcn_s_setprio(0); }
+            sync(2 * t + 1);
+            if (act) soft(t);
+        }
+        sync(2 * ntiles);
+        if (act) { __builtin_amdgcn_s_setprio(1); gemm_pv(ntiles); __builtin_amdgcn_s_setprio(0); }
+        sync(2 * ntiles + 1);
+    } else {
+        sync(0);
+        sync(1);
+        if (act) { __builtin_amdgcn_s_setprio(1); gemm_s(0); __builtin_amdgcn_s_setprio(0); }
+        for (int t = 1; t < ntiles; ++t) {
+            sync(2 * t);
+            if (act) soft(t - 1);
+            sync(2 * t + 1);
+            if (act) { __builtin_amdgcn_s_setprio(1); gemm(t); __builtin_amdgcn_s_setprio(0); }
+        }
+        sync(2 * ntiles);
+        if (act) soft(ntiles - 1);
+        sync(2 * ntiles + 1);
+        if (act) { __builtin_amdgcn_s_setprio(1); gemm_pv(ntiles); __builtin_amdgcn_s_setprio(0); }
+    }
+
+    // ---- output rows
+    const float l_tot = pair_sum(rs.l);
+    if (valid) {
+        const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+        __bf16 *orow = (__bf16 *)p.out + ((int64_t)tok * p.n_q_heads + head) * D;
+#pragma unroll
+        for (int mt = 0; mt < D / 32; ++mt)
+#pragma unroll
+            for (int q4 = 0; q4 < 4; ++q4) {
+                u32x2 v;
+                v[0] = pack_bf16x2(rs.o[mt][4 * q4] * inv, rs.o[mt][4 * q4 + 1] * inv);
+                v[1] = pack_bf16x2(rs.o[mt][4 * q4 + 2] * inv, rs.o[mt][4 * q4 + 3] * inv);
+                *(u32x2 *)(orow + 32 * mt + 8 * q4 + 4 * grp) = v;
+            }
+    }
+
+    // ---- cache rows of the tokens whose first query row is in this workgroup
+    const int own_lo = (row0 + G - 1) / G;
+    const int own_hi = row_last / G;               // inclusive
+    const int n_own = own_hi >= own_lo ? own_hi - own_lo + 1 : 0;
+    unsigned char *kc = (unsigned char *)p.kc_out + ((int64_t)g * p.cap) * ROWB;
+    unsigned char *vc = (unsigned char *)p.vc_out + ((int64_t)g * p.cap) * ROWB;
+    for (int idx = tid; idx < n_own * 16; idx += PP_THREADS) {
+        const int tk = own_lo + (idx >> 4);
+        const int c = 16 * (idx & 15);
+        const uint64_t src = (uint64_t)tk * (uint64_t)nstride_b + c;
+        *(u32x4 *)(kc + (int64_t)tk * ROWB + c) = *(const u32x4 *)(kn_a + src);
+        *(u32x4 *)(vc + (int64_t)tk * ROWB + c) = *(const u32x4 *)(vn_a + src);
+    }
+}
+
+}  // namespace
+
+hipError_t launch_attn_pp(const AttnParams &p, int grid, hipStream_t s) {
+    hipLaunchKernelGGL(attn_pp_kernel, dim3(grid), dim3(PP_THREADS), 0, s, p);
+    return hipGetLastError();
+}
+
+}  // namespace kvr

@@ -29,6 +29,9 @@ bool use_cont(const kvr_desc *d, int64_t S) {
     return d->dtype == KVR_BF16 && d->head_dim == 128 && (int64_t)(d->n_q_heads / d->n_kv_heads) * S <= kContMaxRows;
 }
 
+// Prefill at bf16 / head_dim 128 uses the two-group kernel.
+bool use_pp(const kvr_desc *d) { return d->dtype == KVR_BF16 && d->head_dim == 128; }
+
 bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
 
 int check_desc(const kvr_desc *d) {
@@ -147,6 +150,10 @@ int launch_single(const kvr_desc *d, int mode, const void *Q, const void *K, con
     if (mode == kModeContinue && use_cont(d, n_tok)) {
         const int nct = (int)((rows + 31) / 32);
         e = launch_attn_cont(p, nct, (int)grid, stream);
+    } else if (mode == kModePrefill && use_pp(d)) {
+        const int64_t pp_tiles = (rows + kRowsPP - 1) / kRowsPP;
+        p.tiles_total = (int32_t)pp_tiles;
+        e = launch_attn_pp(p, (int)(pp_tiles * p.n_kv_heads), stream);
     } else if (d->dtype == KVR_BF16) {
         e = launch_attn_bf16(p, d->head_dim, mode, (int)grid, stream);
     } else {
