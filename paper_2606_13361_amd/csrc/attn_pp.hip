@@ -38,6 +38,9 @@ constexpr int STAGE = 2 * TILE;           // 32 KB
 constexpr int NS = 4;                     // ring stages: 128 KB of LDS
 constexpr int PP_THREADS = 512;
 constexpr int PP_LOADS = 4;               // direct loads per wave per tile (2 K + 2 V)
+// a lane's weights of one tile summing to at most 2^kRescaleSlack are each at most that
+constexpr float kSlackSum = 256.f;
+static_assert(kSlackSum == (float)(1 << (int)kRescaleSlack), "slack sum must match the rescale slack");
 
 __device__ __forceinline__ int swz(int row) { return ((row >> 2) & 3) | ((row & 3) << 2); }
 
@@ -93,6 +96,19 @@ __global__ __launch_bounds__(PP_THREADS) void attn_pp_kernel(const AttnParams p)
         lchunk[i] = 16u * (uint32_t)((lane & 15) ^ swz(lrow[i]));
         off_n[i] = (uint32_t)(lrow[i] * nstride_b) + lchunk[i];
     }
+    // load q (0..3) of this wave's four for tile t: K row groups 0, 1, then V row groups 0, 1
+    auto dma_part = [=](int t, int q) {
+        const int k0 = t * KEYS;
+        const int i = q & 1;
+        const unsigned char *dst = smem + (t % NS) * STAGE + 8 * wave * ROWB + (q >> 1) * TILE + 1024 * i;
+        const uint64_t base = (q >> 1) ? vn_a : kn_a;
+        if (k0 + KEYS <= ke) {
+            dma16_s(base + (uint64_t)k0 * nstride_b, off_n[i], dst);
+        } else {
+            const int key = min(k0 + lrow[i], ke - 1);
+            dma16((const void *)(base + (uint64_t)key * (uint64_t)nstride_b + lchunk[i]), dst);
+        }
+    };
     auto load_tile = [=](int t) {
         const int k0 = t * KEYS;
         const unsigned char *kd = smem + (t % NS) * STAGE + 8 * wave * ROWB;
@@ -184,7 +200,7 @@ __global__ __launch_bounds__(PP_THREADS) void attn_pp_kernel(const AttnParams p)
 #pragma unroll
         for (int idx = 0; idx < 16; ++idx) pv(vfrag(vs_, idx), idx);
     };
-    auto gemm = [&](int t) {              // both
+    auto gemm = [&](int t, int dt) {      // both; issues the loads of tile dt (if >= 0) between chunks
         const unsigned char *ks_ = smem + (t % NS) * STAGE;
         const unsigned char *vs_ = smem + ((t + NS - 1) % NS) * STAGE + TILE;
         s_zero();
@@ -202,6 +218,7 @@ __global__ __launch_bounds__(PP_THREADS) void attn_pp_kernel(const AttnParams p)
             pv(v0, 2 * c);
             sm(k1, 1, c);
             pv(v1, 2 * c + 1);
+            if ((c & 1) && dt >= 0) dma_part(dt, c >> 1);
             __builtin_amdgcn_sched_barrier(0);
             if (c + 1 < 8) {
                 k0 = nk0; k1 = nk1; v0 = nv0; v1 = nv1;
@@ -209,7 +226,7 @@ __global__ __launch_bounds__(PP_THREADS) void attn_pp_kernel(const AttnParams p)
         }
     };
     // SOFT(t): causal mask, row max, lazy rescale of (O, l), P_t = 2^(S c2 - m)
-    auto soft = [&](int t) {
+    auto soft = [&](int t, int dt) {      // issues the loads of tile dt (if >= 0) among the exps
         const int k0 = t * KEYS;
         if (k0 + KEYS > k_full) {
             const int lim = max(-1, min(pos - k0, KEYS));
@@ -221,48 +238,60 @@ __global__ __launch_bounds__(PP_THREADS) void attn_pp_kernel(const AttnParams p)
                     if (o > lim) s[st][i] = -INFINITY;
                 }
         }
-        // row max as a tree (5 dependent levels instead of a 32-long chain)
-        float v[32];
+        // P against the current reference m first; the row maximum is needed
+        // only when some lane's weights sum above 2^kRescaleSlack (then one of
+        // them may exceed it) -- the first tile (m = -1e30) always, later tiles
+        // almost never
+        auto exps = [&](int dtl) {
+            float lsum[4] = {0.f, 0.f, 0.f, 0.f};   // four independent partial sums
 #pragma unroll
-        for (int i = 0; i < 16; ++i) {
-            v[i] = s[0][i];
-            v[16 + i] = s[1][i];
-        }
+            for (int st = 0; st < 2; ++st)
 #pragma unroll
-        for (int w = 16; w >= 1; w >>= 1)
+                for (int i = 0; i < 16; i += 2) {
+                    const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[st][i], c2, -rs.m));
+                    const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[st][i + 1], c2, -rs.m));
+                    const uint32_t pk = pack_bf16x2(p0, p1);
+                    float &acc = lsum[(i >> 1) & 3];
+                    acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, pk), kOnes, acc, false);
+                    pf[st][i >> 3][(i & 7) >> 1] = pk;
+                    if ((i & 7) == 6 && dtl >= 0) dma_part(dtl, 2 * st + (i >> 3));
+                }
+            return (lsum[0] + lsum[1]) + (lsum[2] + lsum[3]);
+        };
+        float part = exps(dt);
+        if (__ballot(!(part <= kSlackSum))) {
+            // row max as a tree (5 dependent levels)
+            float v[32];
 #pragma unroll
-            for (int i = 0; i < w; ++i) v[i] = fmaxf(v[i], v[i + w]);
-        const float mx = pair_max(v[0]) * c2;
-        const bool need = mx > rs.m + kRescaleSlack;
-        if (__ballot(need)) {
-            const float m_new = need ? mx : rs.m;
-            const float alpha = __builtin_amdgcn_exp2f(rs.m - m_new);
-            rs.m = m_new;
-            rs.l *= alpha;
-#pragma unroll
-            for (int mt = 0; mt < D / 32; ++mt)
-#pragma unroll
-                for (int i = 0; i < 16; ++i) rs.o[mt][i] *= alpha;
-        }
-        // four independent partial sums of the bf16 weights
-        float lsum[4] = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int st = 0; st < 2; ++st)
-#pragma unroll
-            for (int i = 0; i < 16; i += 2) {
-                const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[st][i], c2, -rs.m));
-                const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[st][i + 1], c2, -rs.m));
-                const uint32_t pk = pack_bf16x2(p0, p1);
-                float &acc = lsum[(i >> 1) & 3];
-                acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, pk), kOnes, acc, false);
-                pf[st][i >> 3][(i & 7) >> 1] = pk;
+            for (int i = 0; i < 16; ++i) {
+                v[i] = s[0][i];
+                v[16 + i] = s[1][i];
             }
-        rs.l += (lsum[0] + lsum[1]) + (lsum[2] + lsum[3]);
+#pragma unroll
+            for (int w = 16; w >= 1; w >>= 1)
+#pragma unroll
+                for (int i = 0; i < w; ++i) v[i] = fmaxf(v[i], v[i + w]);
+            const float mx = pair_max(v[0]) * c2;
+            const bool need = mx > rs.m + kRescaleSlack;
+            if (__ballot(need)) {
+                const float m_new = need ? mx : rs.m;
+                const float alpha = __builtin_amdgcn_exp2f(rs.m - m_new);
+                rs.m = m_new;
+                rs.l *= alpha;
+#pragma unroll
+                for (int mt = 0; mt < D / 32; ++mt)
+#pragma unroll
+                    for (int i = 0; i < 16; ++i) rs.o[mt][i] *= alpha;
+                part = exps(-1);
+            }
+        }
+        rs.l += part;
     };
 
     // ---- steps.  Phase 2t starts once tile t has landed (each wave waits for its
-    // own loads, then the barrier) and issues tile t+2, whose stage held tile t-2
-    // and was last read in phase 2t-1.  Group A: GEMM(t) in phase 2t, SOFT(t)
+    // own loads, then the barrier); during phase 2t every wave issues its loads
+    // of tile t+2, spread through its step, into the stage that held tile t-2
+    // (last read in phase 2t-1).  Group A: GEMM(t) in phase 2t, SOFT(t)
     // in phase 2t+1; group B one phase later.  Both run 2*ntiles + 2 phases.
     auto sync = [&](int phi) {
         __builtin_amdgcn_sched_barrier(0);
@@ -272,7 +301,6 @@ __global__ __launch_bounds__(PP_THREADS) void attn_pp_kernel(const AttnParams p)
             else wait_vmcnt<0>();
             __builtin_amdgcn_s_barrier();
             asm volatile("" ::: "memory");
-            if (t + 2 < ntiles) load_tile(t + 2);
         } else {
             __builtin_amdgcn_s_barrier();
             asm volatile("" ::: "memory");
@@ -282,32 +310,46 @@ __global__ __launch_bounds__(PP_THREADS) void attn_pp_kernel(const AttnParams p)
     load_tile(0);
     if (ntiles > 1) load_tile(1);
     const bool act = wave_active;
+    auto next = [&](int t) { return t + 2 < ntiles ? t + 2 : -1; };   // tile issued in phase 2t
     if (gw == 0) {
         sync(0);
         if (act) { __builtin_amdgcn_s_setprio(1); gemm_s(0); __builtin_amdgcn_s_setprio(0); }
+        if (next(0) >= 0) load_tile(next(0));
         sync(1);
-        if (act) soft(0);
+        if (act) soft(0, -1);
         for (int t = 1; t < ntiles; ++t) {
             sync(2 * t);
-            if (act) { __builtin_amdgcn_s_setprio(1); gemm(t); __builtin_amdgcn_s_setprio(0); }
+            if (act) {
+                __builtin_amdgcn_s_setprio(1);
+                gemm(t, next(t));
+                __builtin_amdgcn_s_setprio(0);
+            } else if (next(t) >= 0) {
+                load_tile(next(t));
+            }
             sync(2 * t + 1);
-            if (act) soft(t);
+            if (act) soft(t, -1);
         }
         sync(2 * ntiles);
         if (act) { __builtin_amdgcn_s_setprio(1); gemm_pv(ntiles); __builtin_amdgcn_s_setprio(0); }
         sync(2 * ntiles + 1);
     } else {
         sync(0);
+        if (next(0) >= 0) load_tile(next(0));
         sync(1);
         if (act) { __builtin_amdgcn_s_setprio(1); gemm_s(0); __builtin_amdgcn_s_setprio(0); }
         for (int t = 1; t < ntiles; ++t) {
             sync(2 * t);
-            if (act) soft(t - 1);
+            if (act) soft(t - 1, next(t));
+            else if (next(t) >= 0) load_tile(next(t));
             sync(2 * t + 1);
-            if (act) { __builtin_amdgcn_s_setprio(1); gemm(t); __builtin_amdgcn_s_setprio(0); }
+            if (act) {
+                __builtin_amdgcn_s_setprio(1);
+                gemm(t, -1);
+                __builtin_amdgcn_s_setprio(0);
+            }
         }
         sync(2 * ntiles);
-        if (act) soft(ntiles - 1);
+        if (act) soft(ntiles - 1, -1);
         sync(2 * ntiles + 1);
         if (act) { __builtin_amdgcn_s_setprio(1); gemm_pv(ntiles); __builtin_amdgcn_s_setprio(0); }
     }
