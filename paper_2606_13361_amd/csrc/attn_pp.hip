@@ -22,7 +22,8 @@
 // c ^ swz(r) (conflict-free K reads and transposing V reads).
 //
 // The workgroup holding the first query row of a token also copies that
-// token's K/V rows into the cache, after its attention work.
+// token's K/V rows into the cache, from the tiles still in LDS after its
+// attention work; output rows leave through LDS as full 256-byte rows.
 #include "attn_common.hpp"
 
 namespace kvr {
@@ -354,11 +355,35 @@ __global__ __launch_bounds__(PP_THREADS) void attn_pp_kernel(const AttnParams p)
         if (act) { __builtin_amdgcn_s_setprio(1); gemm_pv(ntiles); __builtin_amdgcn_s_setprio(0); }
     }
 
-    // ---- output rows
+    // ---- epilogue.  After this barrier no wave reads the ring any more; the
+    // last NS tiles are still in it.
+    __syncthreads();
+
+    // cache rows of the tokens whose first query row is in this workgroup, copied
+    // from the ring: those tokens are the workgroup's last keys (at most 256/G + 1
+    // of them, aligned so that they lie within the last four tiles)
+    const int own_lo = (row0 + G - 1) / G;
+    const int own_hi = row_last / G;               // inclusive, = ke - 1
+    const int n_own = own_hi >= own_lo ? own_hi - own_lo + 1 : 0;
+    unsigned char *kc = (unsigned char *)p.kc_out + ((int64_t)g * p.cap) * ROWB;
+    unsigned char *vc = (unsigned char *)p.vc_out + ((int64_t)g * p.cap) * ROWB;
+    for (int idx = tid; idx < n_own * 32; idx += PP_THREADS) {
+        const int tk = own_lo + (idx >> 5);
+        const int half = (idx >> 4) & 1;             // 0: K row, 1: V row
+        const int c = idx & 15;
+        const int r = tk & (KEYS - 1);
+        const unsigned char *src = smem + ((tk / KEYS) % NS) * STAGE + half * TILE + r * ROWB + 16 * (c ^ swz(r));
+        *(u32x4 *)((half ? vc : kc) + (int64_t)tk * ROWB + 16 * c) = *(const u32x4 *)src;
+    }
+    __syncthreads();
+
+    // output rows through LDS: the wave's 32 rows in bf16 (pitch OPITCH), then 16
+    // bytes per lane, 4 rows (one token's 4 heads for G = 4: 1 KB) per store
+    constexpr int OPITCH = ROWB + 16;
     const float l_tot = pair_sum(rs.l);
-    if (valid) {
+    if (wave_active) {
+        unsigned char *ob = smem + wave * 32 * OPITCH;
         const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
-        __bf16 *orow = (__bf16 *)p.out + ((int64_t)tok * p.n_q_heads + head) * D;
 #pragma unroll
         for (int mt = 0; mt < D / 32; ++mt)
 #pragma unroll
@@ -366,22 +391,19 @@ __global__ __launch_bounds__(PP_THREADS) void attn_pp_kernel(const AttnParams p)
                 u32x2 v;
                 v[0] = pack_bf16x2(rs.o[mt][4 * q4] * inv, rs.o[mt][4 * q4 + 1] * inv);
                 v[1] = pack_bf16x2(rs.o[mt][4 * q4 + 2] * inv, rs.o[mt][4 * q4 + 3] * inv);
-                *(u32x2 *)(orow + 32 * mt + 8 * q4 + 4 * grp) = v;
+                *(u32x2 *)(ob + j * OPITCH + 2 * (32 * mt + 8 * q4 + 4 * grp)) = v;
             }
-    }
-
-    // ---- cache rows of the tokens whose first query row is in this workgroup
-    const int own_lo = (row0 + G - 1) / G;
-    const int own_hi = row_last / G;               // inclusive
-    const int n_own = own_hi >= own_lo ? own_hi - own_lo + 1 : 0;
-    unsigned char *kc = (unsigned char *)p.kc_out + ((int64_t)g * p.cap) * ROWB;
-    unsigned char *vc = (unsigned char *)p.vc_out + ((int64_t)g * p.cap) * ROWB;
-    for (int idx = tid; idx < n_own * 16; idx += PP_THREADS) {
-        const int tk = own_lo + (idx >> 4);
-        const int c = 16 * (idx & 15);
-        const uint64_t src = (uint64_t)tk * (uint64_t)nstride_b + c;
-        *(u32x4 *)(kc + (int64_t)tk * ROWB + c) = *(const u32x4 *)(kn_a + src);
-        *(u32x4 *)(vc + (int64_t)tk * ROWB + c) = *(const u32x4 *)(vn_a + src);
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // this wave's rows are in LDS
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const int rr = 4 * i + (lane >> 4);
+            const int rw = wrow0 + rr;
+            if (rw < R) {
+                const u32x4 v = *(const u32x4 *)(ob + rr * OPITCH + 16 * (lane & 15));
+                __bf16 *orow = (__bf16 *)p.out + ((int64_t)(rw / G) * p.n_q_heads + g * G + rw % G) * D;
+                *(u32x4 *)(orow + 8 * (lane & 15)) = v;
+            }
+        }
     }
 }
 
