@@ -206,10 +206,10 @@ def main():
     digest = kernel_source_digest()
     traffic = measured_traffic(digest)
     roofs = {
-        "readers": {"kernel": "attn_stream_readers_kernel", "bound": "mfma", "achieved": round(rd_tflops, 2),
+        "readers": {"kernel": "attn_pp_kernel<readers>", "bound": "mfma", "achieved": round(rd_tflops, 2),
                     "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(rd_tflops / PEAK_BF16_TFLOPS, 4),
                     "work_per_launch": rd_flops, "avg_launch_ms": round(avg["readers"] * 1e3, 4)},
-        "prefill": {"kernel": "attn_bf16_kernel<128, prefill>", "bound": "mfma", "achieved": round(pf_tflops, 2),
+        "prefill": {"kernel": "attn_pp_kernel<prefill>", "bound": "mfma", "achieved": round(pf_tflops, 2),
                     "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(pf_tflops / PEAK_BF16_TFLOPS, 4),
                     "work_per_launch": pf_flops, "avg_launch_ms": round(avg["prefill"] * 1e3, 4)},
         "continue": {"kernel": "attn_cont_kernel<3> + merge_bf16_kernel<128>", "bound": "hbm",

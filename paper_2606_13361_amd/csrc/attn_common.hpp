@@ -38,6 +38,9 @@ constexpr int THREADS = 256;
 // P and fp32 sums hold as well as p <= 1, and the O rescale is skipped for
 // almost every tile.
 constexpr float kRescaleSlack = 8.f;
+// A lane's weights of one tile summing to at most 2^kRescaleSlack are each at
+// most that: the test that lets a tile skip the row maximum.
+constexpr float kSlackSum = 256.f;
 
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
     // v_cvt_pk_bf16_f32: round to nearest even

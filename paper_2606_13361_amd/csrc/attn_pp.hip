@@ -1,5 +1,5 @@
-// attn_pp.hip -- prefill, bf16, head_dim 128: the two-group ("ping-pong")
-// member of the attention family.
+// attn_pp.hip -- prefill and many readers, bf16, head_dim 128: the two-group
+// ("ping-pong") member of the attention family.
 //
 // A workgroup is 8 waves, 2 per SIMD, holding 256 query rows of one kv head
 // (32 rows per wave, GQA-packed as everywhere in the family).  Waves 0-3 form
@@ -39,12 +39,11 @@ constexpr int STAGE = 2 * TILE;           // 32 KB
 constexpr int NS = 4;                     // ring stages: 128 KB of LDS
 constexpr int PP_THREADS = 512;
 constexpr int PP_LOADS = 4;               // direct loads per wave per tile (2 K + 2 V)
-// a lane's weights of one tile summing to at most 2^kRescaleSlack are each at most that
-constexpr float kSlackSum = 256.f;
 static_assert(kSlackSum == (float)(1 << (int)kRescaleSlack), "slack sum must match the rescale slack");
 
 __device__ __forceinline__ int swz(int row) { return ((row >> 2) & 3) | ((row & 3) << 2); }
 
+template <int MODE>
 __global__ __launch_bounds__(PP_THREADS) void attn_pp_kernel(const AttnParams p) {
     __shared__ __attribute__((aligned(1024))) unsigned char smem[NS * STAGE];
 
@@ -55,29 +54,36 @@ __global__ __launch_bounds__(PP_THREADS) void attn_pp_kernel(const AttnParams p)
     const int j = lane & 31;
     const int grp = lane >> 5;
 
-    // ---- work: kv head fastest (XCD locality), row tiles longest first
+    // ---- work: kv head fastest (XCD locality); prefill row tiles longest first.
+    // Keys are the cached prefix [0, npre) (readers) followed by the segment's own
+    // rows; prefill has no prefix.
     const int G = p.group;
     const int g = blockIdx.x % p.n_kv_heads;
-    const int tile = p.tiles_total - 1 - blockIdx.x / p.n_kv_heads;
-    const int L = p.seg_tok0[1];
-    const int R = G * L;
-    const int row0 = tile * kRowsPP;
+    const int tile_lin = MODE == kModePrefill ? p.tiles_total - 1 - blockIdx.x / p.n_kv_heads
+                                              : blockIdx.x / p.n_kv_heads;
+    const int seg = MODE == kModeReaders ? find_segment(p, tile_lin) : 0;
+    const int tok0 = p.seg_tok0[seg];
+    const int R = G * (p.seg_tok0[seg + 1] - tok0);
+    const int row0 = (tile_lin - p.seg_tile0[seg]) * kRowsPP;
     const int row_last = min(row0 + kRowsPP, R) - 1;
-    const int ke = row_last / G + 1;                              // keys any row here may see
+    const int npre = MODE == kModePrefill ? 0 : (int)p.n_prefix;
+    const int ke = npre + row_last / G + 1;                       // keys any row here may see
     const int ntiles = (ke + KEYS - 1) / KEYS;
 
-    const int r = row0 + wave * 32 + j;
+    // rows 32*slot .. +31 of the tile, slot 2*(wave & 3) + group: a partial tile
+    // keeps both waves of a SIMD busy as long as it can
+    const int wrow0 = row0 + 32 * (2 * (wave & 3) + gw);
+    const int r = wrow0 + j;
     const bool valid = r < R;
     const int tok = valid ? r / G : 0;
     const int head = g * G + (valid ? r % G : 0);
-    const int pos = valid ? tok : -1;
-    const int wrow0 = row0 + wave * 32;
+    const int pos = valid ? npre + tok : -1;
     const bool wave_active = wrow0 < R;
-    const int k_full = wave_active ? wrow0 / G + 1 : 0;          // keys every row of this wave sees
+    const int k_full = wave_active ? npre + wrow0 / G + 1 : 0;   // keys every row of this wave sees
 
     u32x4 qf[D / 16];
     {
-        const __bf16 *qrow = (const __bf16 *)p.q + ((int64_t)tok * p.n_q_heads + head) * D;
+        const __bf16 *qrow = (const __bf16 *)p.q + ((int64_t)(tok0 + tok) * p.n_q_heads + head) * D;
 #pragma unroll
         for (int ks = 0; ks < D / 16; ++ks)
             qf[ks] = valid ? *(const u32x4 *)(qrow + 16 * ks + 8 * grp) : (u32x4){0, 0, 0, 0};
@@ -87,49 +93,43 @@ __global__ __launch_bounds__(PP_THREADS) void attn_pp_kernel(const AttnParams p)
     // 4 rows per instruction; lane -> row 8w + 4i + lane/16, LDS slot lane%16,
     // global chunk slot ^ swz(row)
     const int64_t nstride_b = (int64_t)p.n_kv_heads * ROWB;
-    const uint64_t kn_a = (uint64_t)(uintptr_t)p.kn + (uint64_t)g * ROWB;
-    const uint64_t vn_a = (uint64_t)(uintptr_t)p.vn + (uint64_t)g * ROWB;
+    // new rows of this segment (key npre + i is row tok0 + i), cached rows of head g
+    const uint64_t kn_a = (uint64_t)(uintptr_t)p.kn + (uint64_t)tok0 * nstride_b + (uint64_t)g * ROWB;
+    const uint64_t vn_a = (uint64_t)(uintptr_t)p.vn + (uint64_t)tok0 * nstride_b + (uint64_t)g * ROWB;
+    const uint64_t kc_a = (uint64_t)(uintptr_t)p.kc + (uint64_t)g * p.cap * ROWB;
+    const uint64_t vc_a = (uint64_t)(uintptr_t)p.vc + (uint64_t)g * p.cap * ROWB;
     int lrow[2];
-    uint32_t lchunk[2], off_n[2];
+    uint32_t lchunk[2], off_n[2], off_c[2];
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
         lrow[i] = 8 * wave + 4 * i + (lane >> 4);
         lchunk[i] = 16u * (uint32_t)((lane & 15) ^ swz(lrow[i]));
         off_n[i] = (uint32_t)(lrow[i] * nstride_b) + lchunk[i];
+        off_c[i] = (uint32_t)(lrow[i] * ROWB) + lchunk[i];
     }
     // load q (0..3) of this wave's four for tile t: K row groups 0, 1, then V row groups 0, 1
     auto dma_part = [=](int t, int q) {
         const int k0 = t * KEYS;
         const int i = q & 1;
         const unsigned char *dst = smem + (t % NS) * STAGE + 8 * wave * ROWB + (q >> 1) * TILE + 1024 * i;
-        const uint64_t base = (q >> 1) ? vn_a : kn_a;
-        if (k0 + KEYS <= ke) {
-            dma16_s(base + (uint64_t)k0 * nstride_b, off_n[i], dst);
+        const uint64_t nbase = (q >> 1) ? vn_a : kn_a;
+        const uint64_t cbase = (q >> 1) ? vc_a : kc_a;
+        if (k0 + KEYS <= npre) {                               // all rows cached
+            dma16_s(cbase + (uint64_t)k0 * ROWB, off_c[i], dst);
+        } else if (k0 >= npre && k0 + KEYS <= ke) {            // all rows new
+            dma16_s(nbase + (uint64_t)(k0 - npre) * nstride_b, off_n[i], dst);
         } else {
+            // prefix/new boundary or ragged end: per-row source, rows past ke repeat
+            // row ke-1 (beyond every causal bound, masked)
             const int key = min(k0 + lrow[i], ke - 1);
-            dma16((const void *)(base + (uint64_t)key * (uint64_t)nstride_b + lchunk[i]), dst);
+            const uint64_t off = key < npre ? (uint64_t)key * ROWB : (uint64_t)(key - npre) * (uint64_t)nstride_b;
+            const uint64_t sel = 0 - (uint64_t)(key < npre);   // base select by mask
+            dma16((const void *)(((cbase & sel) | (nbase & ~sel)) + off + lchunk[i]), dst);
         }
     };
     auto load_tile = [=](int t) {
-        const int k0 = t * KEYS;
-        const unsigned char *kd = smem + (t % NS) * STAGE + 8 * wave * ROWB;
-        const unsigned char *vd = kd + TILE;
-        if (k0 + KEYS <= ke) {
-            const uint64_t kb_ = kn_a + (uint64_t)k0 * nstride_b, vb_ = vn_a + (uint64_t)k0 * nstride_b;
 #pragma unroll
-            for (int i = 0; i < 2; ++i) dma16_s(kb_, off_n[i], kd + 1024 * i);
-#pragma unroll
-            for (int i = 0; i < 2; ++i) dma16_s(vb_, off_n[i], vd + 1024 * i);
-        } else {
-            // ragged last tile: rows past ke repeat row ke-1 (beyond every causal bound, masked)
-#pragma unroll
-            for (int i = 0; i < 2; ++i) {
-                const int key = min(k0 + lrow[i], ke - 1);
-                const uint64_t off = (uint64_t)key * (uint64_t)nstride_b + lchunk[i];
-                dma16((const void *)(kn_a + off), kd + 1024 * i);
-                dma16((const void *)(vn_a + off), vd + 1024 * i);
-            }
-        }
+        for (int q = 0; q < PP_LOADS; ++q) dma_part(t, q);
     };
 
     // ---- read maps (per lane, loop invariant); as in the streamed kernel
@@ -359,6 +359,7 @@ __global__ __launch_bounds__(PP_THREADS) void attn_pp_kernel(const AttnParams p)
     // last NS tiles are still in it.
     __syncthreads();
 
+    if constexpr (MODE == kModePrefill) {
     // cache rows of the tokens whose first query row is in this workgroup, copied
     // from the ring: those tokens are the workgroup's last keys (at most 256/G + 1
     // of them, aligned so that they lie within the last four tiles)
@@ -376,6 +377,7 @@ __global__ __launch_bounds__(PP_THREADS) void attn_pp_kernel(const AttnParams p)
         *(u32x4 *)((half ? vc : kc) + (int64_t)tk * ROWB + 16 * c) = *(const u32x4 *)src;
     }
     __syncthreads();
+    }
 
     // output rows through LDS: the wave's 32 rows in bf16 (pitch OPITCH), then 16
     // bytes per lane, 4 rows (one token's 4 heads for G = 4: 1 KB) per store
@@ -400,7 +402,7 @@ __global__ __launch_bounds__(PP_THREADS) void attn_pp_kernel(const AttnParams p)
             const int rw = wrow0 + rr;
             if (rw < R) {
                 const u32x4 v = *(const u32x4 *)(ob + rr * OPITCH + 16 * (lane & 15));
-                __bf16 *orow = (__bf16 *)p.out + ((int64_t)(rw / G) * p.n_q_heads + g * G + rw % G) * D;
+                __bf16 *orow = (__bf16 *)p.out + ((int64_t)(tok0 + rw / G) * p.n_q_heads + g * G + rw % G) * D;
                 *(u32x4 *)(orow + 8 * (lane & 15)) = v;
             }
         }
@@ -409,8 +411,11 @@ __global__ __launch_bounds__(PP_THREADS) void attn_pp_kernel(const AttnParams p)
 
 }  // namespace
 
-hipError_t launch_attn_pp(const AttnParams &p, int grid, hipStream_t s) {
-    hipLaunchKernelGGL(attn_pp_kernel, dim3(grid), dim3(PP_THREADS), 0, s, p);
+hipError_t launch_attn_pp(const AttnParams &p, int mode, int grid, hipStream_t s) {
+    if (mode == kModePrefill)
+        hipLaunchKernelGGL(attn_pp_kernel<kModePrefill>, dim3(grid), dim3(PP_THREADS), 0, s, p);
+    else
+        hipLaunchKernelGGL(attn_pp_kernel<kModeReaders>, dim3(grid), dim3(PP_THREADS), 0, s, p);
     return hipGetLastError();
 }
 

@@ -20,16 +20,13 @@ constexpr int64_t kTargetWorkgroupsStaged = 512;
 constexpr int64_t kTargetWorkgroupsCont = 256;   // split-K-in-workgroup kernel: one per CU (155 KB of LDS)
 constexpr int64_t kMinSplitKeys = 256;
 
-// The streamed kernel serves bf16, head_dim 128 many-readers calls.
-bool use_stream(const kvr_desc *d) { return d->dtype == KVR_BF16 && d->head_dim == 128; }
-
 // Continuations of at most kContMaxRows query rows per kv head (decode steps,
 // short suffixes) at bf16 / head_dim 128 use the kernel whose waves split the keys.
 bool use_cont(const kvr_desc *d, int64_t S) {
     return d->dtype == KVR_BF16 && d->head_dim == 128 && (int64_t)(d->n_q_heads / d->n_kv_heads) * S <= kContMaxRows;
 }
 
-// Prefill at bf16 / head_dim 128 uses the two-group kernel.
+// Prefill and many readers at bf16 / head_dim 128 use the two-group kernel.
 bool use_pp(const kvr_desc *d) { return d->dtype == KVR_BF16 && d->head_dim == 128; }
 
 bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
@@ -153,7 +150,7 @@ int launch_single(const kvr_desc *d, int mode, const void *Q, const void *K, con
     } else if (mode == kModePrefill && use_pp(d)) {
         const int64_t pp_tiles = (rows + kRowsPP - 1) / kRowsPP;
         p.tiles_total = (int32_t)pp_tiles;
-        e = launch_attn_pp(p, (int)(pp_tiles * p.n_kv_heads), stream);
+        e = launch_attn_pp(p, kModePrefill, (int)(pp_tiles * p.n_kv_heads), stream);
     } else if (d->dtype == KVR_BF16) {
         e = launch_attn_bf16(p, d->head_dim, mode, (int)grid, stream);
     } else {
@@ -265,7 +262,7 @@ int kvr_continue_batched(const kvr_desc *desc, const void *Qs, const void *Ks, c
         return KVR_ERR_ALIGN;
 
     const int64_t G = desc->n_q_heads / desc->n_kv_heads;
-    const int rpt = rows_per_tile(desc);
+    const int rpt = use_pp(desc) ? kRowsPP : rows_per_tile(desc);
     for (int32_t first = 0; first < n; first += kMaxSegments) {
         const int32_t cnt = (n - first) < kMaxSegments ? (n - first) : kMaxSegments;
         AttnParams p;
@@ -289,7 +286,7 @@ int kvr_continue_batched(const kvr_desc *desc, const void *Qs, const void *Ks, c
         p.tiles_total = tiles;
         p.rows_total = 0;
         const int64_t grid = (int64_t)tiles * p.n_kv_heads;
-        hipError_t e = use_stream(desc) ? launch_attn_stream_readers(p, (int)grid, (hipStream_t)stream)
+        hipError_t e = use_pp(desc) ? launch_attn_pp(p, kModeReaders, (int)grid, (hipStream_t)stream)
                        : desc->dtype == KVR_BF16 ? launch_attn_bf16(p, desc->head_dim, kModeReaders, (int)grid,
                                                                     (hipStream_t)stream)
                                                : launch_attn_f32(p, desc->head_dim, (int)grid, (hipStream_t)stream);

@@ -60,13 +60,10 @@ enum { kModePrefill = 0, kModeContinue = 1, kModeReaders = 2 };
 // bf16 path (MFMA), D in {64, 128}
 hipError_t launch_attn_bf16(const AttnParams &p, int head_dim, int mode, int grid, hipStream_t s);
 hipError_t launch_merge_bf16(const MergeParams &p, int head_dim, hipStream_t s);
-// bf16 streamed path (direct-to-LDS tile pipeline), D = 128, many readers
-constexpr int kStreamStagesReaders = 2;    // x 64 keys (32 KB): 64 KB of LDS, two workgroups per CU
-constexpr int kStreamSubReaders = 2;
-hipError_t launch_attn_stream_readers(const AttnParams &p, int grid, hipStream_t s);
-// bf16 prefill at D = 128: two groups of 4 waves alternate matrix and softmax steps
+// bf16 prefill and many readers at D = 128: two groups of 4 waves alternate
+// matrix and softmax steps
 constexpr int kRowsPP = 256;   // query rows per workgroup (8 waves x 32)
-hipError_t launch_attn_pp(const AttnParams &p, int grid, hipStream_t s);
+hipError_t launch_attn_pp(const AttnParams &p, int mode, int grid, hipStream_t s);
 // bf16 continuation for G*S <= 96 rows (D = 128): waves split the keys
 constexpr int kContMaxRows = 96;
 hipError_t launch_attn_cont(const AttnParams &p, int ncol_tiles, int grid, hipStream_t s);
