@@ -47,6 +47,18 @@ def continue_bytes(L_prefix, S, n_q_heads, n_kv_heads, head_dim, elt):
     return cache + new_q + new_kv + out
 
 
+def q8_artifact_bytes(tokens, n_kv_heads, head_dim, layers=1):
+    """Bytes of the int8 artifact: one byte per cached K/V element plus two fp32
+    scales (K and V) per layer."""
+    return kv_bytes_per_token(n_kv_heads, head_dim, 1, layers) * tokens + 2 * 4 * layers
+
+
+def continue_q8_bytes(L_prefix, S, n_q_heads, n_kv_heads, head_dim):
+    """Continuation over the int8 artifact: int8 cache rows, bf16 new rows and output."""
+    cache = kv_bytes_per_token(n_kv_heads, head_dim, 1) * L_prefix
+    return cache + continue_bytes(0, S, n_q_heads, n_kv_heads, head_dim, 2)
+
+
 def prefill_bytes(n, n_q_heads, n_kv_heads, head_dim, elt):
     q_out = 2 * n * n_q_heads * head_dim * elt
     kv_in = 2 * n * n_kv_heads * head_dim * elt
