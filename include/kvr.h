@@ -50,7 +50,7 @@
 extern "C" {
 #endif
 
-#define KVR_ABI_VERSION 1
+#define KVR_ABI_VERSION 2
 
 typedef enum {
     KVR_OK = 0,
@@ -131,6 +131,52 @@ int kvr_continue_batched(const kvr_desc *desc, const void *Qs, const void *Ks, c
  */
 int kvr_cache_append(const kvr_desc *desc, const void *Ks, const void *Vs, int64_t S,
                      void *kcache, void *vcache, int64_t L_cur, void *stream);
+
+/*
+ * The int8 KV artifact (paper, Section "Quantizing the artifact: size vs.
+ * exactness": the context KV stored at per-tensor symmetric int8, half the
+ * bytes of the 16-bit artifact, no longer token-exact).
+ *   One scale per tensor: s_K = max|K| / 127 over every kv head and cached row
+ *   [0, L) (fp32, correctly rounded; 1 for an all-zero tensor), likewise s_V.
+ *   Code of x: clamp(round-half-even(x / s), -127, 127), the quotient in fp32.
+ *   Layouts (bytes; P = capacity rounded up to a multiple of 32, head_dim 128):
+ *     kq  [n_kv_heads][P][128]: row j of kv head g holds the code of K[g][j][d]
+ *         at byte 64 * ((d >> 3) & 1) + 8 * (d >> 4) + (d & 7) of the row
+ *     vq  [n_kv_heads][P / 32][128][32]: the code of V[g][32 b + k][d] is byte
+ *         ((g * (P / 32) + b) * 128 + d) * 32 + pos(k), with
+ *         pos(k) = 16 * ((k >> 2) & 1) + 8 * (k >> 4) + 4 * ((k >> 3) & 1) + (k & 3)
+ *     scales  float[2] = {s_K, s_V} in device memory
+ *   These are the operand orders of the continuation kernel's matrix products,
+ *   so it reads every code with plain 16-byte loads.  The artifact is read
+ *   only; a decode chain continues over it and keeps its new rows in bf16.
+ */
+
+/* Bytes of kq (and of vq) for this descriptor; (size_t)-1 if it is invalid. */
+size_t kvr_q8_bytes(const kvr_desc *desc);
+
+/*
+ * Quantize cache rows [0, L) of every kv head (bf16 kcache/vcache) into the
+ * int8 artifact: writes kq/vq rows [0, L) plus the zero codes up to the next
+ * multiple of 32, and scales.  Needs bf16 (KVR_ERR_DTYPE), head_dim 128
+ * (KVR_ERR_SHAPE), L <= capacity.  kq and vq hold kvr_q8_bytes(desc) bytes
+ * each and are 16-byte aligned; scales needs 4-byte alignment.  Runs four
+ * small kernels on `stream` (scales first hold the maxima).
+ */
+int kvr_quantize_cache(const kvr_desc *desc, const void *kcache, const void *vcache, int64_t L,
+                       void *kq, void *vq, float *scales, void *stream);
+
+/*
+ * Continuation of S tokens over the int8 artifact: kvr_continue with the
+ * cached rows [0, L_prefix) replaced by their dequantized values code * s;
+ * the new tokens' Ks/Vs stay bf16.  The artifact must come from
+ * kvr_quantize_cache with the same descriptor and some L >= L_prefix.
+ * Supported: bf16, head_dim 128 and (n_q_heads / n_kv_heads) * S <= 96
+ * (decode steps and short continuations); KVR_ERR_SHAPE otherwise.
+ * ws as for kvr_continue (kvr_workspace_bytes(desc, L_prefix, S, 1)).
+ */
+int kvr_continue_q8(const kvr_desc *desc, const void *Qs, const void *Ks, const void *Vs,
+                    const void *kq, const void *vq, const float *scales, int64_t L_prefix,
+                    int64_t S, void *out, void *ws, size_t ws_bytes, void *stream);
 
 /*
  * Workspace bytes a continuation needs: n <= 1 for kvr_continue with

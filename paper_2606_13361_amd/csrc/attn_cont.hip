@@ -21,6 +21,8 @@
 // LDS tile layout as in the streamed kernel: 256-byte rows, 16-byte chunk c of
 // row r in slot c ^ swz(r), conflict-free for the K reads and the
 // transposing V reads.
+#include <type_traits>
+
 #include "attn_common.hpp"
 
 namespace kvr {
@@ -126,7 +128,36 @@ __device__ __forceinline__ void finish_quarter(const AttnParams &p, const RowSta
     }
 }
 
-template <int NCT>
+// int8 artifact stages: 32 keys of K codes (32 rows x 128 B) at the slot
+// start, the 32-key block of V codes (128 head-dim rows x 32 B) at +HALF.
+// 16-byte chunk c of K row r sits in slot c ^ swzk(r), chunk h of V row d in
+// slot h ^ swzv(d): the 16-lane groups of the fragment reads below then touch
+// 16 distinct bank groups.
+__device__ __forceinline__ int swzk(int row) { return (row >> 1) & 7; }
+__device__ __forceinline__ int swzv(int d) { return (d >> 3) & 1; }
+constexpr int LOADS_Q8 = 8;                  // direct loads per int8 stage (4 K + 4 V)
+
+// 16 int8 codes -> two MFMA operands of 8 bf16 each (exact: |code| <= 127)
+__device__ __forceinline__ void codes_to_bf16(const u32x4 w, u32x4 &lo, u32x4 &hi) {
+    uint32_t o[8];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const int32_t x = (int32_t)w[q];
+        const float f0 = (float)((x << 24) >> 24), f1 = (float)((x << 16) >> 24);
+        const float f2 = (float)((x << 8) >> 24), f3 = (float)(x >> 24);
+        o[2 * q] = pack_bf16x2(f0, f1);
+        o[2 * q + 1] = pack_bf16x2(f2, f3);
+    }
+    lo = (u32x4){o[0], o[1], o[2], o[3]};
+    hi = (u32x4){o[4], o[5], o[6], o[7]};
+}
+
+// Q8 = false: cache and new rows are bf16.  Q8 = true: the cached rows come
+// from the int8 artifact (kq/vq codes, scales s_K, s_V): scores of cached keys
+// are scaled by s_K inside the softmax exponent, the cached part of O by s_V
+// before the first new key (or at the end); the new rows stay bf16.  Cached
+// and new keys then never share a stage.
+template <int NCT, bool Q8>
 __global__ __launch_bounds__(THREADS) void attn_cont_kernel(const AttnParams p) {
     __shared__ __attribute__((aligned(1024))) unsigned char smem[LDS_BYTES];
 
@@ -143,10 +174,11 @@ __global__ __launch_bounds__(THREADS) void attn_cont_kernel(const AttnParams p) 
     const int R = G * S;                            // <= 32 * NCT
     const int64_t npre = p.n_prefix;
     const int64_t k_all = npre + S;
+    const bool last_split = split == p.nsplit - 1;
     int64_t kb = 0, ke = k_all;
     if (p.nsplit > 1) {
         kb = (int64_t)split * p.chunk;
-        ke = (split == p.nsplit - 1) ? k_all : min(kb + p.chunk, npre);
+        ke = last_split ? k_all : min(kb + p.chunk, npre);
     }
 
     // ---- rows: column tile c, lane column j -> row 32*c + j
@@ -161,9 +193,16 @@ __global__ __launch_bounds__(THREADS) void attn_cont_kernel(const AttnParams p) 
         head[c] = g * G + (valid[c] ? r % G : 0);
         pos[c] = valid[c] ? npre + tok[c] : -1;
     }
-    // ---- this wave's stages and its load map (instruction i moves rows 4*i + lane/16)
-    const int nst = ke > kb ? (int)((ke - kb + SKEYS - 1) / SKEYS) : 0;
+    // ---- stages.  bf16: 32-key stages over [kb, ke).  Q8: n_cst stages of cached
+    // keys [kb, ce) (the last one may reach past npre: masked), then the new rows'
+    // stages (last split only).  Wave w takes stages w, w+4, ...
+    const int64_t ce = ke < npre ? ke : npre;
+    const int n_cst = Q8 ? (ce > kb ? (int)((ce - kb + SKEYS - 1) / SKEYS) : 0) : 0;
+    const int nst = Q8 ? n_cst + ((p.nsplit == 1 || last_split) ? (S + SKEYS - 1) / SKEYS : 0)
+                       : (ke > kb ? (int)((ke - kb + SKEYS - 1) / SKEYS) : 0);
     const int my_n = nst > wave ? (nst - wave + 3) / 4 : 0;
+    auto is_q8 = [&](int t) { return Q8 && wave + 4 * t < n_cst; };
+
     const int64_t nstride_b = (int64_t)p.n_kv_heads * ROWB;
     const unsigned char *kc0 = (const unsigned char *)p.kc + (int64_t)g * p.cap * ROWB;
     const unsigned char *vc0 = (const unsigned char *)p.vc + (int64_t)g * p.cap * ROWB;
@@ -176,16 +215,40 @@ __global__ __launch_bounds__(THREADS) void attn_cont_kernel(const AttnParams p) 
         lchunk[i] = 16u * (uint32_t)((lane & 15) ^ swz(row));
         off_c[i] = (uint32_t)row * ROWB + lchunk[i];
     }
-    const int64_t cache_end = ke < npre ? ke : npre;
+    // int8 load maps: K instruction i moves rows 8i + lane/8, V instruction i head-dim
+    // rows 32i + lane/2
+    uint32_t offk[4], offv[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int row = 8 * i + (lane >> 3);
+        offk[i] = (uint32_t)row * D + 16u * (uint32_t)((lane & 7) ^ swzk(row));
+        const int d = 32 * i + (lane >> 1);
+        offv[i] = (uint32_t)d * 32 + 16u * (uint32_t)((lane & 1) ^ swzv(d));
+    }
+    const int64_t padded = (p.cap + 31) / 32 * 32;
+    const uint64_t kq_a = (uint64_t)(uintptr_t)p.kc + (uint64_t)g * padded * D;   // Q8: artifact
+    const uint64_t vq_a = (uint64_t)(uintptr_t)p.vc + (uint64_t)g * padded * D;
+    const int64_t cache_end = ce;
     // addresses as integers: no pointer selects, nothing left in private memory
     const uint64_t kc_a = (uint64_t)(uintptr_t)kc0, vc_a = (uint64_t)(uintptr_t)vc0;
     const uint64_t kn_a = (uint64_t)(uintptr_t)kn0, vn_a = (uint64_t)(uintptr_t)vn0;
     const uint32_t ring_lds = (uint32_t)(wave * RING);
     auto load_stage = [=](int t) {
-        const int64_t key0 = kb + (int64_t)(wave + 4 * t) * SKEYS;
+        const int i_st = wave + 4 * t;
         const unsigned char *kd = smem + ring_lds + (t % NSW) * STAGE;
         const unsigned char *vd = kd + HALF;
-        if (key0 + SKEYS <= cache_end) {
+        if (Q8 && i_st < n_cst) {
+            const int64_t key0 = kb + (int64_t)i_st * SKEYS;                   // a multiple of 32
+            const uint64_t kb_ = kq_a + (uint64_t)key0 * D, vb_ = vq_a + (uint64_t)key0 * D;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) dma16_s(kb_, offk[i], kd + 1024 * i);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) dma16_s(vb_, offv[i], vd + 1024 * i);
+            return;
+        }
+        // bf16 keys: key0 is absolute (bf16 path) or npre + the new row index (Q8)
+        const int64_t key0 = Q8 ? npre + (int64_t)(i_st - n_cst) * SKEYS : kb + (int64_t)i_st * SKEYS;
+        if (!Q8 && key0 + SKEYS <= cache_end) {
             const uint64_t kb_ = kc_a + (uint64_t)key0 * ROWB, vb_ = vc_a + (uint64_t)key0 * ROWB;
 #pragma unroll
             for (int i = 0; i < 8; ++i) dma16_s(kb_, off_c[i], kd + 1024 * i);
@@ -228,6 +291,11 @@ __global__ __launch_bounds__(THREADS) void attn_cont_kernel(const AttnParams p) 
 #pragma unroll
     for (int c = 0; c < NCT; ++c) rs[c].zero();
     const float c2 = p.scale_log2;
+    float c2q = c2, s_v = 1.f;
+    if (Q8) {
+        c2q = c2 * p.qscale[0];
+        s_v = p.qscale[1];
+    }
 
     // Q rows of all column tiles into LDS (swizzled like K, rows past R repeat
     // row R-1: their columns are computed and never stored), then this wave's
@@ -248,25 +316,47 @@ __global__ __launch_bounds__(THREADS) void attn_cont_kernel(const AttnParams p) 
     }
     if (my_n > 0) {
         load_stage(0);
-        wait_vmcnt<LOADS>();
+        if (is_q8(0)) wait_vmcnt<LOADS_Q8>();
+        else wait_vmcnt<LOADS>();
     } else {
         wait_vmcnt<0>();
     }
     __builtin_amdgcn_s_barrier();       // all of Q is in LDS
     asm volatile("" ::: "memory");
 
-    for (int t = 0; t < my_n; ++t) {
+    bool o_scaled = !Q8;                // Q8: cached part of O still in code units of V
+    auto scale_o = [&]() {
+#pragma unroll
+        for (int c = 0; c < NCT; ++c)
+#pragma unroll
+            for (int mt = 0; mt < D / 32; ++mt)
+#pragma unroll
+                for (int i = 0; i < 16; ++i) rs[c].o[mt][i] *= s_v;
+        o_scaled = true;
+    };
+
+    // one stage; the kind (int8 codes or bf16 rows) is a compile-time tag, so the
+    // int8 stages and the bf16 stages run in loops of their own
+    auto stage = [&](auto kind, int t) {
+        constexpr bool q8 = decltype(kind)::value;
         asm volatile("" ::: "memory");
         if (t + 1 < my_n) {
             load_stage(t + 1);          // its slot held stage t-1, consumed last iteration
-            wait_vmcnt<LOADS>();        // stage t landed, stage t+1 in flight
+            if (is_q8(t + 1)) wait_vmcnt<LOADS_Q8>();   // stage t landed, stage t+1 in flight
+            else wait_vmcnt<LOADS>();
         } else {
             wait_vmcnt<0>();
         }
         asm volatile("" ::: "memory");
-        const int64_t key0 = kb + (int64_t)(wave + 4 * t) * SKEYS;
+        const int i_st = wave + 4 * t;
+        // absolute key of the stage's first row
+        const int64_t key0 = Q8 ? (q8 ? kb + (int64_t)i_st * SKEYS : npre + (int64_t)(i_st - n_cst) * SKEYS)
+                                : kb + (int64_t)i_st * SKEYS;
         const unsigned char *ks_ = smem + ring_lds + (t % NSW) * STAGE;
         const unsigned char *vs_ = ks_ + HALF;
+        if constexpr (Q8 && !q8) {
+            if (!o_scaled) scale_o();
+        }
 
         // S^T for every column tile: each K fragment feeds NCT chains
         f32x16 s[NCT];
@@ -274,22 +364,41 @@ __global__ __launch_bounds__(THREADS) void attn_cont_kernel(const AttnParams p) 
         for (int c = 0; c < NCT; ++c)
 #pragma unroll
             for (int i = 0; i < 16; ++i) s[c][i] = 0.f;
+        if constexpr (q8) {
+            // lane (j, grp): codes of row j, head-dim steps 2 pr and 2 pr + 1
 #pragma unroll
-        for (int ks = 0; ks < D / 16; ++ks) {
-            const u32x4 a = *(const u32x4 *)(ks_ + ka[ks]);
+            for (int pr = 0; pr < 4; ++pr) {
+                const u32x4 w = *(const u32x4 *)(ks_ + j * D + 16 * ((4 * grp + pr) ^ swzk(j)));
+                u32x4 a0, a1;
+                codes_to_bf16(w, a0, a1);
 #pragma unroll
-            for (int c = 0; c < NCT; ++c) {
-                // Q row 32*c + j has the same swizzle as row j
-                const u32x4 b = *(const u32x4 *)(qlds + 32 * c * ROWB + ka[ks]);
-                s[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a), as_bf16x8(b), s[c], 0, 0, 0);
+                for (int c = 0; c < NCT; ++c) {
+                    const u32x4 b0 = *(const u32x4 *)(qlds + 32 * c * ROWB + ka[2 * pr]);
+                    const u32x4 b1 = *(const u32x4 *)(qlds + 32 * c * ROWB + ka[2 * pr + 1]);
+                    s[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a0), as_bf16x8(b0), s[c], 0, 0, 0);
+                    s[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a1), as_bf16x8(b1), s[c], 0, 0, 0);
+                }
+            }
+        } else {
+#pragma unroll
+            for (int ks = 0; ks < D / 16; ++ks) {
+                const u32x4 a = *(const u32x4 *)(ks_ + ka[ks]);
+#pragma unroll
+                for (int c = 0; c < NCT; ++c) {
+                    // Q row 32*c + j has the same swizzle as row j
+                    const u32x4 b = *(const u32x4 *)(qlds + 32 * c * ROWB + ka[ks]);
+                    s[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a), as_bf16x8(b), s[c], 0, 0, 0);
+                }
             }
         }
+        const float c2s = q8 ? c2q : c2;
         u32x4 pf[NCT][2];
 #pragma unroll
         for (int c = 0; c < NCT; ++c) {
-            // causal mask: only stages reaching past the first continuation row's position
-            if (key0 + SKEYS > npre + 1) {
-                const int64_t lim64 = pos[c] - key0;
+            // mask: keys past a row's causal bound (new rows) or past the cached
+            // prefix (an int8 stage reaching beyond npre)
+            if (key0 + SKEYS > npre + 1 || (q8 && key0 + SKEYS > npre)) {
+                const int64_t lim64 = (q8 ? npre - 1 : pos[c]) - key0;
                 const int lim = lim64 < -1 ? -1 : (lim64 > SKEYS ? SKEYS : (int)lim64);
 #pragma unroll
                 for (int i = 0; i < 16; ++i) {
@@ -300,7 +409,7 @@ __global__ __launch_bounds__(THREADS) void attn_cont_kernel(const AttnParams p) 
             float mx = -INFINITY;
 #pragma unroll
             for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s[c][i]);
-            mx = pair_max(mx) * c2;
+            mx = pair_max(mx) * c2s;
             const bool need = mx > rs[c].m + kRescaleSlack;
             if (__ballot(need)) {
                 const float m_new = need ? mx : rs[c].m;
@@ -315,8 +424,8 @@ __global__ __launch_bounds__(THREADS) void attn_cont_kernel(const AttnParams p) 
             float lsum = 0.f;
 #pragma unroll
             for (int i = 0; i < 16; i += 2) {
-                const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[c][i], c2, -rs[c].m));
-                const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[c][i + 1], c2, -rs[c].m));
+                const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[c][i], c2s, -rs[c].m));
+                const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[c][i + 1], c2s, -rs[c].m));
                 const uint32_t pk = pack_bf16x2(p0, p1);
                 lsum = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, pk), kOnes, lsum, false);
                 pf[c][i >> 3][(i & 7) >> 1] = pk;
@@ -324,23 +433,47 @@ __global__ __launch_bounds__(THREADS) void attn_cont_kernel(const AttnParams p) 
             rs[c].l += lsum;
         }
         // O^T += V^T P^T: each V^T fragment feeds NCT chains
-#pragma unroll
-        for (int kk = 0; kk < 2; ++kk)
+        if constexpr (q8) {
+            // lane (j, grp): codes of head-dim row 32 mt + j, key slots of half kk = 0 and 1
 #pragma unroll
             for (int mt = 0; mt < D / 32; ++mt) {
-                const unsigned char *va0 = vs_ + va[0][mt] + 16 * kk * ROWB;
-                const unsigned char *va1 = vs_ + va[1][mt] + 16 * kk * ROWB;
-                const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)va0);
-                const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)va1);
-                const u32x2 lo2 = __builtin_bit_cast(u32x2, lo);
-                const u32x2 hi2 = __builtin_bit_cast(u32x2, hi);
-                const u32x4 a = {lo2[0], lo2[1], hi2[0], hi2[1]};
+                const int d = 32 * mt + j;
+                const u32x4 w = *(const u32x4 *)(vs_ + d * 32 + 16 * (grp ^ swzv(d)));
+                u32x4 a0, a1;
+                codes_to_bf16(w, a0, a1);
 #pragma unroll
-                for (int c = 0; c < NCT; ++c)
-                    rs[c].o[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a), as_bf16x8(pf[c][kk]),
+                for (int c = 0; c < NCT; ++c) {
+                    rs[c].o[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a0), as_bf16x8(pf[c][0]),
                                                                          rs[c].o[mt], 0, 0, 0);
+                    rs[c].o[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a1), as_bf16x8(pf[c][1]),
+                                                                         rs[c].o[mt], 0, 0, 0);
+                }
             }
+        } else {
+#pragma unroll
+            for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+                for (int mt = 0; mt < D / 32; ++mt) {
+                    const unsigned char *va0 = vs_ + va[0][mt] + 16 * kk * ROWB;
+                    const unsigned char *va1 = vs_ + va[1][mt] + 16 * kk * ROWB;
+                    const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)va0);
+                    const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)va1);
+                    const u32x2 lo2 = __builtin_bit_cast(u32x2, lo);
+                    const u32x2 hi2 = __builtin_bit_cast(u32x2, hi);
+                    const u32x4 a = {lo2[0], lo2[1], hi2[0], hi2[1]};
+#pragma unroll
+                    for (int c = 0; c < NCT; ++c)
+                        rs[c].o[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a), as_bf16x8(pf[c][kk]),
+                                                                             rs[c].o[mt], 0, 0, 0);
+                }
+        }
+    };
+    int t = 0;
+    if constexpr (Q8) {
+        for (; t < my_n && is_q8(t); ++t) stage(std::true_type{}, t);
     }
+    for (; t < my_n; ++t) stage(std::false_type{}, t);
+    if (Q8 && !o_scaled) scale_o();
 
     // ---- merge: post (m, l) and the non-owned O quarters, one barrier, then
     // wave w finishes head-dim quarter w
@@ -376,11 +509,19 @@ __global__ __launch_bounds__(THREADS) void attn_cont_kernel(const AttnParams p) 
 
 }  // namespace
 
-hipError_t launch_attn_cont(const AttnParams &p, int ncol_tiles, int grid, hipStream_t s) {
-    switch (ncol_tiles) {
-        case 1: hipLaunchKernelGGL(attn_cont_kernel<1>, dim3(grid), dim3(THREADS), 0, s, p); break;
-        case 2: hipLaunchKernelGGL(attn_cont_kernel<2>, dim3(grid), dim3(THREADS), 0, s, p); break;
-        default: hipLaunchKernelGGL(attn_cont_kernel<3>, dim3(grid), dim3(THREADS), 0, s, p); break;
+hipError_t launch_attn_cont(const AttnParams &p, int ncol_tiles, bool q8, int grid, hipStream_t s) {
+    if (q8) {
+        switch (ncol_tiles) {
+            case 1: hipLaunchKernelGGL((attn_cont_kernel<1, true>), dim3(grid), dim3(THREADS), 0, s, p); break;
+            case 2: hipLaunchKernelGGL((attn_cont_kernel<2, true>), dim3(grid), dim3(THREADS), 0, s, p); break;
+            default: hipLaunchKernelGGL((attn_cont_kernel<3, true>), dim3(grid), dim3(THREADS), 0, s, p); break;
+        }
+    } else {
+        switch (ncol_tiles) {
+            case 1: hipLaunchKernelGGL((attn_cont_kernel<1, false>), dim3(grid), dim3(THREADS), 0, s, p); break;
+            case 2: hipLaunchKernelGGL((attn_cont_kernel<2, false>), dim3(grid), dim3(THREADS), 0, s, p); break;
+            default: hipLaunchKernelGGL((attn_cont_kernel<3, false>), dim3(grid), dim3(THREADS), 0, s, p); break;
+        }
     }
     return hipGetLastError();
 }

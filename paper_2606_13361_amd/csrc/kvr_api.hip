@@ -109,9 +109,10 @@ int append_impl(const kvr_desc *d, const void *Ks, const void *Vs, int64_t S, vo
 
 // mode kModePrefill: kc/vc are the caches to fill (bf16: in the attention
 // kernel itself); kModeContinue: kc/vc are the cached prefix (read only).
+// qscale != NULL: continuation over the int8 artifact (kc/vc are its codes).
 int launch_single(const kvr_desc *d, int mode, const void *Q, const void *K, const void *V, void *kc,
                   void *vc, int64_t n_prefix, int64_t n_tok, void *out, const Split &sp, void *ws,
-                  hipStream_t stream) {
+                  hipStream_t stream, const float *qscale = nullptr) {
     AttnParams p;
     fill_common(p, d);
     p.q = Q; p.kn = K; p.vn = V; p.out = out;
@@ -124,6 +125,7 @@ int launch_single(const kvr_desc *d, int mode, const void *Q, const void *K, con
         p.vc = vc;
     }
     p.ws = (float *)ws;
+    p.qscale = qscale;
     p.n_prefix = n_prefix;
     p.nsplit = sp.nsplit;
     p.chunk = sp.chunk;
@@ -146,7 +148,7 @@ int launch_single(const kvr_desc *d, int mode, const void *Q, const void *K, con
     hipError_t e;
     if (mode == kModeContinue && use_cont(d, n_tok)) {
         const int nct = (int)((rows + 31) / 32);
-        e = launch_attn_cont(p, nct, (int)grid, stream);
+        e = launch_attn_cont(p, nct, qscale != nullptr, (int)grid, stream);
     } else if (mode == kModePrefill && use_pp(d)) {
         const int64_t pp_tiles = (rows + kRowsPP - 1) / kRowsPP;
         p.tiles_total = (int32_t)pp_tiles;
@@ -235,6 +237,57 @@ int kvr_continue(const kvr_desc *desc, const void *Qs, const void *Ks, const voi
         return KVR_ERR_ALIGN;
     return launch_single(desc, kModeContinue, Qs, Ks, Vs, (void *)kcache, (void *)vcache, L_prefix, S, out,
                          sp, ws, (hipStream_t)stream);
+}
+
+size_t kvr_q8_bytes(const kvr_desc *desc) {
+    if (check_desc(desc) != KVR_OK) return (size_t)-1;
+    const int64_t padded = (desc->capacity + 31) / 32 * 32;
+    return (size_t)desc->n_kv_heads * (size_t)padded * (size_t)desc->head_dim;
+}
+
+int kvr_quantize_cache(const kvr_desc *desc, const void *kcache, const void *vcache, int64_t L, void *kq,
+                       void *vq, float *scales, void *stream) {
+    int st = check_desc(desc);
+    if (st) return st;
+    if (desc->dtype != KVR_BF16) return KVR_ERR_DTYPE;
+    if (desc->head_dim != 128) return KVR_ERR_SHAPE;
+    if (L < 0 || L > kMaxKeys) return KVR_ERR_SHAPE;
+    if (L > desc->capacity) return KVR_ERR_CAPACITY;
+    if (L == 0) return KVR_OK;
+    if (!kcache || !vcache || !kq || !vq || !scales) return KVR_ERR_NULL;
+    if (!aligned16(kcache) || !aligned16(vcache) || !aligned16(kq) || !aligned16(vq) || ((uintptr_t)scales & 3u))
+        return KVR_ERR_ALIGN;
+    QuantParams q;
+    q.kc = kcache; q.vc = vcache; q.kq = kq; q.vq = vq; q.scales = scales;
+    q.L = L; q.cap = desc->capacity; q.padded = (desc->capacity + 31) / 32 * 32;
+    q.n_kv_heads = desc->n_kv_heads;
+    return launch_quantize(q, (hipStream_t)stream) == hipSuccess ? KVR_OK : KVR_ERR_DEVICE;
+}
+
+int kvr_continue_q8(const kvr_desc *desc, const void *Qs, const void *Ks, const void *Vs, const void *kq,
+                    const void *vq, const float *scales, int64_t L_prefix, int64_t S, void *out, void *ws,
+                    size_t ws_bytes, void *stream) {
+    int st = check_desc(desc);
+    if (st) return st;
+    if (desc->dtype != KVR_BF16) return KVR_ERR_DTYPE;
+    if (L_prefix < 0 || S < 0 || S > kMaxTokens || L_prefix > kMaxKeys) return KVR_ERR_SHAPE;
+    if (desc->head_dim != 128 || !use_cont(desc, S)) return KVR_ERR_SHAPE;
+    if (L_prefix > desc->capacity) return KVR_ERR_CAPACITY;
+    if (S == 0) return KVR_OK;
+    if (!Qs || !Ks || !Vs || !out) return KVR_ERR_NULL;
+    if (L_prefix > 0 && (!kq || !vq || !scales)) return KVR_ERR_NULL;
+    const Split sp = plan_split(desc, L_prefix, S);
+    if (ws_bytes < sp.ws_bytes) return KVR_ERR_WORKSPACE;
+    if (sp.ws_bytes > 0 && !ws) return KVR_ERR_NULL;
+    if (!aligned16(Qs) || !aligned16(Ks) || !aligned16(Vs) || !aligned16(out) || !aligned16(kq) ||
+        !aligned16(vq) || !aligned16(ws) || ((uintptr_t)scales & 3u))
+        return KVR_ERR_ALIGN;
+    // without a prefix there is nothing quantized: a plain continuation
+    if (L_prefix == 0)
+        return launch_single(desc, kModeContinue, Qs, Ks, Vs, nullptr, nullptr, 0, S, out, sp, ws,
+                             (hipStream_t)stream);
+    return launch_single(desc, kModeContinue, Qs, Ks, Vs, (void *)kq, (void *)vq, L_prefix, S, out, sp, ws,
+                         (hipStream_t)stream, scales);
 }
 
 int kvr_continue_batched(const kvr_desc *desc, const void *Qs, const void *Ks, const void *Vs,

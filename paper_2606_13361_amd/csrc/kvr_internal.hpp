@@ -24,6 +24,7 @@ struct AttnParams {
     void *kc_out;    // prefill: cache the new K rows go to [n_kv_heads][cap][D]
     void *vc_out;
     float *ws;       // split partials: O [nsplit][Hkv][rows][D], then (m, l) [nsplit][Hkv][rows][2]
+    const float *qscale;   // int8 artifact continuation: {s_K, s_V} (kc/vc then point at the codes)
     int64_t cap;
     int64_t n_prefix;  // cached keys, positions [0, n_prefix); every query row sees them all
     int64_t chunk;     // prefix keys per split, a multiple of the key tile
@@ -49,6 +50,17 @@ struct AppendParams {
     int32_t row_chunks;  // 16-byte chunks per row (D * elt / 16)
 };
 
+// Quantization of cache rows [0, L) into the int8 artifact (layouts in kvr.h)
+struct QuantParams {
+    const void *kc;   // bf16 [n_kv_heads][cap][128]
+    const void *vc;
+    void *kq;         // int8 artifact, padded rows per head
+    void *vq;
+    float *scales;    // [2]: maxima while the kernels run, then {s_K, s_V}
+    int64_t L, cap, padded;
+    int32_t n_kv_heads;
+};
+
 struct MergeParams {
     const float *ws;
     void *out;
@@ -66,7 +78,9 @@ constexpr int kRowsPP = 256;   // query rows per workgroup (8 waves x 32)
 hipError_t launch_attn_pp(const AttnParams &p, int mode, int grid, hipStream_t s);
 // bf16 continuation for G*S <= 96 rows (D = 128): waves split the keys
 constexpr int kContMaxRows = 96;
-hipError_t launch_attn_cont(const AttnParams &p, int ncol_tiles, int grid, hipStream_t s);
+hipError_t launch_attn_cont(const AttnParams &p, int ncol_tiles, bool q8, int grid, hipStream_t s);
+// int8 artifact
+hipError_t launch_quantize(const QuantParams &p, hipStream_t s);
 // fp32 path (VALU), D in {64, 128}
 hipError_t launch_attn_f32(const AttnParams &p, int head_dim, int grid, hipStream_t s);
 // cache write

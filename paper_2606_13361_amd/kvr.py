@@ -20,7 +20,8 @@ KVR_ERR_CAPACITY, KVR_ERR_WORKSPACE, KVR_ERR_ALIGN, KVR_ERR_DEVICE = 4, 5, 6, 7
 KVR_BF16, KVR_F32 = 0, 1
 
 EXPORTS = ("kvr_prefill", "kvr_continue", "kvr_continue_batched", "kvr_cache_append",
-           "kvr_workspace_bytes", "kvr_strerror", "kvr_abi_version")
+           "kvr_workspace_bytes", "kvr_strerror", "kvr_abi_version",
+           "kvr_q8_bytes", "kvr_quantize_cache", "kvr_continue_q8")
 
 _TORCH_DTYPE = {KVR_BF16: torch.bfloat16, KVR_F32: torch.float32}
 
@@ -59,11 +60,15 @@ def load():
     lib.kvr_cache_append.argtypes = [D, P, P, I64, P, P, I64, P]
     lib.kvr_workspace_bytes.argtypes = [D, I64, I64, ctypes.c_int32]
     lib.kvr_workspace_bytes.restype = SZ
+    lib.kvr_q8_bytes.argtypes = [D]
+    lib.kvr_q8_bytes.restype = SZ
+    lib.kvr_quantize_cache.argtypes = [D, P, P, I64, P, P, P, P]
+    lib.kvr_continue_q8.argtypes = [D, P, P, P, P, P, P, I64, I64, P, P, SZ, P]
     lib.kvr_strerror.argtypes = [ctypes.c_int]
     lib.kvr_strerror.restype = ctypes.c_char_p
     lib.kvr_abi_version.argtypes = []
     for f in (lib.kvr_prefill, lib.kvr_continue, lib.kvr_continue_batched, lib.kvr_cache_append,
-              lib.kvr_abi_version):
+              lib.kvr_abi_version, lib.kvr_quantize_cache, lib.kvr_continue_q8):
         f.restype = ctypes.c_int
     _lib = lib
     return lib
@@ -174,6 +179,53 @@ def kvr_cache_append(desc, Ks, Vs, S, kcache, vcache, L_cur, stream=None):
     kc, vc = _cache_ptrs(desc, kcache, vcache, True)
     _raise(load().kvr_cache_append(ctypes.byref(desc), k, v, int(S), kc, vc, int(L_cur), _stream(stream)),
            "kvr_cache_append")
+
+
+def kvr_q8_bytes(desc):
+    """Bytes of each int8 artifact tensor (kq, vq) for this descriptor."""
+    nb = load().kvr_q8_bytes(ctypes.byref(desc))
+    if nb == ctypes.c_size_t(-1).value:
+        raise ValueError("invalid layer descriptor")
+    return nb
+
+
+def q8_artifact(desc, device="cuda"):
+    """Allocate (with torch) an int8 artifact: (kq, vq, scales)."""
+    nb = kvr_q8_bytes(desc)
+    return (torch.empty(nb, dtype=torch.int8, device=device), torch.empty(nb, dtype=torch.int8, device=device),
+            torch.empty(2, dtype=torch.float32, device=device))
+
+
+def _check_q8(desc, kq, vq, scales):
+    nb = kvr_q8_bytes(desc)
+    for t, name in ((kq, "kq"), (vq, "vq")):
+        if not isinstance(t, torch.Tensor) or not t.is_cuda or t.dtype != torch.int8 or not t.is_contiguous():
+            raise ValueError("%s must be a contiguous int8 GPU tensor" % name)
+        if t.numel() != nb:
+            raise ValueError("%s holds %d bytes, the descriptor needs %d" % (name, t.numel(), nb))
+    if (not isinstance(scales, torch.Tensor) or not scales.is_cuda or scales.dtype != torch.float32
+            or scales.numel() != 2 or not scales.is_contiguous()):
+        raise ValueError("scales must be a contiguous float32 GPU tensor of 2 values")
+    return kq.data_ptr(), vq.data_ptr(), scales.data_ptr()
+
+
+def kvr_quantize_cache(desc, kcache, vcache, L, kq, vq, scales, stream=None):
+    kc, vc = _cache_ptrs(desc, kcache, vcache, True)
+    a, b, sc = _check_q8(desc, kq, vq, scales)
+    _raise(load().kvr_quantize_cache(ctypes.byref(desc), kc, vc, int(L), a, b, sc, _stream(stream)),
+           "kvr_quantize_cache")
+
+
+def kvr_continue_q8(desc, Qs, Ks, Vs, kq, vq, scales, L_prefix, S, out, ws=None, stream=None):
+    Hq, Hkv, d = desc.n_q_heads, desc.n_kv_heads, desc.head_dim
+    q = _check(Qs, "Qs", desc, (S, Hq, d))
+    k = _check(Ks, "Ks", desc, (S, Hkv, d))
+    v = _check(Vs, "Vs", desc, (S, Hkv, d))
+    o = _check(out, "out", desc, (S, Hq, d))
+    a, b, sc = _check_q8(desc, kq, vq, scales)
+    wp, wn = _workspace(ws)
+    _raise(load().kvr_continue_q8(ctypes.byref(desc), q, k, v, a, b, sc, int(L_prefix), int(S), o, wp, wn,
+                                  _stream(stream)), "kvr_continue_q8")
 
 
 def _workspace(ws):

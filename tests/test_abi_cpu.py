@@ -36,7 +36,7 @@ def desc(**kw):
 def header_functions():
     text = open(HEADER).read()
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return sorted(set(re.findall(r"\b(kvr_[a-z_]+)\s*\(", text)))
+    return sorted(set(re.findall(r"\b(kvr_[a-z0-9_]+)\s*\(", text)))
 
 
 def exported_symbols(path):
@@ -70,7 +70,7 @@ def test_exports_match_header(lib):
 
 
 def test_abi_version_and_strerror(lib):
-    assert lib.kvr_abi_version() == 1
+    assert lib.kvr_abi_version() == 2
     for code in range(8):
         assert len(lib.kvr_strerror(code)) > 0
     assert b"unknown" in lib.kvr_strerror(99)
@@ -200,3 +200,49 @@ def test_python_binding_rejects_metadata_mismatch():
     x = torch.zeros((2, 4, 64), dtype=torch.float32)
     with pytest.raises(ValueError):
         kvr._check(x, "Q", d, (2, 4, 64))       # CPU tensor and fp32 vs bf16
+
+
+def quant(lib, d, L=64, kc=A, vc=A, kq=A, vq=A, sc=A):
+    return lib.kvr_quantize_cache(ctypes.byref(d), kc, vc, L, kq, vq, sc, None)
+
+
+def cont_q8(lib, d, Lp=64, S=8, Q=A, K=A, V=A, kq=A, vq=A, sc=A, out=A, ws=A, wsb=1 << 30):
+    return lib.kvr_continue_q8(ctypes.byref(d), Q, K, V, kq, vq, sc, Lp, S, out, ws, wsb, None)
+
+
+def test_q8_bytes(lib):
+    assert lib.kvr_q8_bytes(ctypes.byref(desc(capacity=4096))) == 8 * 4096 * 128
+    assert lib.kvr_q8_bytes(ctypes.byref(desc(capacity=33))) == 8 * 64 * 128      # rows padded to 32
+    assert lib.kvr_q8_bytes(ctypes.byref(desc(capacity=0))) == 0
+    assert lib.kvr_q8_bytes(ctypes.byref(desc(head_dim=96))) == ctypes.c_size_t(-1).value
+
+
+def test_quantize_errors(lib):
+    d = desc(capacity=100)
+    assert quant(lib, desc(dtype=kvr.KVR_F32)) == kvr.KVR_ERR_DTYPE
+    assert quant(lib, desc(head_dim=64)) == kvr.KVR_ERR_SHAPE
+    assert quant(lib, d, L=-1) == kvr.KVR_ERR_SHAPE
+    assert quant(lib, d, L=101) == kvr.KVR_ERR_CAPACITY
+    assert quant(lib, d, L=0, kc=None, vc=None, kq=None, vq=None, sc=None) == kvr.KVR_OK
+    for kw in ("kc", "vc", "kq", "vq", "sc"):
+        assert quant(lib, d, **{kw: None}) == kvr.KVR_ERR_NULL, kw
+    for kw in ("kc", "vc", "kq", "vq"):
+        assert quant(lib, d, **{kw: MIS}) == kvr.KVR_ERR_ALIGN, kw
+    assert quant(lib, d, sc=A + 2) == kvr.KVR_ERR_ALIGN
+
+
+def test_continue_q8_errors(lib):
+    d = desc(capacity=100)
+    assert cont_q8(lib, desc(dtype=kvr.KVR_F32)) == kvr.KVR_ERR_DTYPE
+    assert cont_q8(lib, desc(head_dim=64)) == kvr.KVR_ERR_SHAPE
+    assert cont_q8(lib, d, S=25) == kvr.KVR_ERR_SHAPE           # G * S = 100 > 96 rows
+    assert cont_q8(lib, d, Lp=-1) == kvr.KVR_ERR_SHAPE
+    assert cont_q8(lib, d, Lp=101) == kvr.KVR_ERR_CAPACITY
+    assert cont_q8(lib, d, S=0, Q=None, K=None, V=None, out=None) == kvr.KVR_OK
+    for kw in ("Q", "K", "V", "out", "kq", "vq", "sc"):
+        assert cont_q8(lib, d, **{kw: None}) == kvr.KVR_ERR_NULL, kw
+    for kw in ("Q", "K", "V", "out", "kq", "vq"):
+        assert cont_q8(lib, d, **{kw: MIS}) == kvr.KVR_ERR_ALIGN, kw
+    d2 = desc(capacity=8192)
+    need = lib.kvr_workspace_bytes(ctypes.byref(d2), 4096, 24, 1)
+    assert cont_q8(lib, d2, Lp=4096, S=24, wsb=need - 1) == kvr.KVR_ERR_WORKSPACE
