@@ -342,7 +342,33 @@ def sweep(torch, kvr, A, W, dev, stream, lengths, suffix=None):
         tc = graph_time(torch, stream, lambda: [cont(i) for i in range(R)], R)
         if not torch.equal(oc, ref_out):
             raise RuntimeError("graph replay of the continuation differs from the eager result")
-        del pool
+        # the same continuation over int8 artifacts of the rotated caches (>= 1 GiB of artifacts)
+        nb8 = kvr.kvr_q8_bytes(desc)
+        R8 = max(2, -(-(1 << 30) // (2 * nb8)))
+        arts = []
+        for i in range(R8):
+            kq, vq, sc = kvr.q8_artifact(desc)
+            c = pool[i % R]
+            kvr.kvr_quantize_cache(desc, c[0], c[1], L, kq, vq, sc)
+            arts.append((kq, vq, sc))
+        oc8 = torch.empty_like(qs)
+
+        def cont8(i):
+            kq, vq, sc = arts[i % R8]
+            kvr.kvr_continue_q8(desc, qs, ks, vs, kq, vq, sc, L, S, oc8, ws)
+        for i in range(R8):
+            cont8(i)
+        cont(0)
+        cont8(0)
+        torch.cuda.synchronize()
+        q8_dev = float((oc8.float() - oc.float()).abs().max())   # int8 artifact vs bf16 cache, same inputs
+        cont8(R8 - 1)
+        torch.cuda.synchronize()
+        ref8 = oc8.clone()
+        tc8 = graph_time(torch, stream, lambda: [cont8(i) for i in range(R8)], R8)
+        if not torch.equal(oc8, ref8):
+            raise RuntimeError("graph replay of the int8 continuation differs from the eager result")
+        del pool, arts
         tp_avg = sum(tp) / len(tp)
         tc_avg = tc
         tce_avg = sum(tc_eager) / len(tc_eager)
@@ -361,6 +387,11 @@ def sweep(torch, kvr, A, W, dev, stream, lengths, suffix=None):
             "continue_timing": "HIP-graph replay of %d rotated calls (eager: host-issued, one event pair per call)" % R,
             "reuse_speedup": round(tp_avg / tc_avg, 2),
             "break_even_N": round(A.break_even(tp_avg, tc_avg), 4),
+            "continue_q8_us": round(tc8 * 1e6, 2),
+            "continue_q8_GBps": round(A.continue_q8_bytes(L, S, Hq, Hkv, D) / tc8 / 1e9, 1),
+            "q8_speedup_vs_bf16_cache": round(tc_avg / tc8, 3),
+            "q8_maxabs_vs_bf16_cache": round(q8_dev, 5),
+            "continue_q8_rotated_artifacts": R8,
         })
         del q, k, v, out, kc, vc
         torch.cuda.empty_cache()
