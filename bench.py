@@ -42,6 +42,7 @@ def parse():
     ap.add_argument("--no-sweep", action="store_true")
     ap.add_argument("--no-decode36", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-artifact", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="target CPU-oracle sample time")
     ap.add_argument("--sweep-lengths", type=str, default=None,
                     help="comma-separated prefix lengths for the sweep (default: all four)")
@@ -230,6 +231,8 @@ def main():
         result["sweep"] = sweep(torch, kvr, A, W, dev, stream, lens_, args.sweep_suffix)
     if not args.no_decode36:
         result["decode36"] = decode36(torch, kvr, A, W, dev, stream)
+    if not args.no_artifact:
+        result["artifact"] = artifact(torch, kvr, W, dev, stream)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(q, k, v, A, args.cpu_seconds)
     print(json.dumps(result), flush=True)
@@ -444,6 +447,42 @@ def decode36(torch, kvr, A, W, dev, stream):
                 "(chain_eager_ms: host-issued launches)",
     }
     del caches, qkv
+    torch.cuda.empty_cache()
+    return res
+
+
+def artifact(torch, kvr, W, dev, stream):
+    """The 36-layer artifact of the 3774-token context (Alg. 1 save, Alg. 2 load):
+    device <-> pinned host memory, one strided copy per layer and tensor."""
+    sh = W.QWEN
+    NL, L = W.QWEN_LAYERS, W.LAYER_L
+    desc = kvr.make_desc(sh.n_q_heads, sh.n_kv_heads, sh.head_dim, torch.bfloat16, L + 24)
+    g = torch.Generator(device=dev)
+    g.manual_seed(7)
+    kcs = [torch.randn((sh.n_kv_heads, L + 24, sh.head_dim), generator=g, device=dev).to(torch.bfloat16)
+           for _ in range(NL)]
+    vcs = [torch.randn((sh.n_kv_heads, L + 24, sh.head_dim), generator=g, device=dev).to(torch.bfloat16)
+           for _ in range(NL)]
+    nb = kvr.kvr_artifact_bytes(desc, NL, L)
+    host = torch.empty(nb, dtype=torch.uint8).pin_memory()
+    k2 = [torch.empty_like(x) for x in kcs]
+    v2 = [torch.empty_like(x) for x in vcs]
+    kvr.kvr_artifact_save(desc, "qwen3-4b", kcs, vcs, L, host)
+    kvr.kvr_artifact_load(desc, "qwen3-4b", host, k2, v2)
+    torch.cuda.synchronize()
+    ts = timed(torch, stream, lambda i: kvr.kvr_artifact_save(desc, "qwen3-4b", kcs, vcs, L, host), 3)
+    tl = timed(torch, stream, lambda i: kvr.kvr_artifact_load(desc, "qwen3-4b", host, k2, v2), 3)
+    exact = all(torch.equal(a[:, :L], b[:, :L]) for a, b in zip(kcs + vcs, k2 + v2))
+    t_s, t_l = sorted(ts)[1], sorted(tl)[1]
+    res = {
+        "layers": NL, "tokens": L, "MB": round(nb / 1e6, 2),
+        "save_ms": round(t_s * 1e3, 3), "save_GBps": round(nb / t_s / 1e9, 2),
+        "load_ms": round(t_l * 1e3, 3), "load_GBps": round(nb / t_l / 1e9, 2),
+        "round_trip_exact": exact,
+        "note": "pinned host memory, device <-> host over the host link; the paper's C_load for "
+                "this artifact (Table 1 row 3774 tokens: 557 MB)",
+    }
+    del kcs, vcs, k2, v2, host
     torch.cuda.empty_cache()
     return res
 

@@ -60,7 +60,9 @@ typedef enum {
     KVR_ERR_CAPACITY = 4,  /* the cache rows addressed exceed the capacity         */
     KVR_ERR_WORKSPACE = 5, /* workspace smaller than kvr_workspace_bytes()         */
     KVR_ERR_ALIGN = 6,     /* a device pointer is not 16-byte aligned              */
-    KVR_ERR_DEVICE = 7     /* a HIP call or kernel launch failed                   */
+    KVR_ERR_DEVICE = 7,    /* a HIP call or kernel launch failed                   */
+    KVR_ERR_MISMATCH = 8   /* an artifact's metadata does not match (model, dtype,
+                              heads, head_dim, layers) or its header is not valid  */
 } kvr_status;
 
 typedef enum { KVR_BF16 = 0, KVR_F32 = 1 } kvr_dtype;
@@ -177,6 +179,55 @@ int kvr_quantize_cache(const kvr_desc *desc, const void *kcache, const void *vca
 int kvr_continue_q8(const kvr_desc *desc, const void *Qs, const void *Ks, const void *Vs,
                     const void *kq, const void *vq, const float *scales, int64_t L_prefix,
                     int64_t S, void *out, void *ws, size_t ws_bytes, void *stream);
+
+/*
+ * The KV artifact on the host (paper, Alg. 1 SaveKV and Alg. 2
+ * GenerateFromKV): the per-layer cached K/V rows [0, L) serialized with
+ * metadata m = (model id, dtype, L); the consumer rejects an artifact made for
+ * another (model, dtype).  Layout, little-endian:
+ *   header, KVR_ARTIFACT_HEADER_BYTES bytes:
+ *     char     magic[8]         "KVRART01"
+ *     uint32   version          1
+ *     uint32   header_bytes     256
+ *     char     model_id[128]    NUL-terminated, NUL-padded
+ *     int32    dtype, n_layers, n_kv_heads, head_dim
+ *     int64    length           L, cached rows per kv head
+ *     uint64   payload_bytes    2 * n_layers * n_kv_heads * L * head_dim * element bytes
+ *     80 bytes of zero
+ *   payload: for layer 0, 1, ...: K rows [n_kv_heads][L][head_dim], then V rows
+ *   likewise (the cache rows [0, L) of each kv head, packed).
+ * The copies run on `stream` (device <-> host, one strided copy per layer and
+ * tensor); host memory from hipHostMalloc (or torch pin_memory) makes them
+ * asynchronous at full link speed, pageable memory works but serializes.
+ */
+#define KVR_ARTIFACT_HEADER_BYTES 256
+
+/* Bytes of an artifact of n_layers layers and L rows; (size_t)-1 if invalid. */
+size_t kvr_artifact_bytes(const kvr_desc *desc, int32_t n_layers, int64_t L);
+
+/*
+ * Serialize cache rows [0, L) of n_layers layers into host memory `host`
+ * (host_bytes >= kvr_artifact_bytes, else KVR_ERR_WORKSPACE).  kcaches and
+ * vcaches are HOST arrays of n_layers device pointers to [n_kv_heads][capacity]
+ * [head_dim] caches.  The header is written before the call returns; the rows
+ * are copied on `stream` (synchronize before reading them).  model_id: at most
+ * 127 bytes (KVR_ERR_SHAPE otherwise).
+ */
+int kvr_artifact_save(const kvr_desc *desc, const char *model_id, int32_t n_layers, int64_t L,
+                      const void *const *kcaches, const void *const *vcaches, void *host,
+                      size_t host_bytes, void *stream);
+
+/*
+ * Load an artifact from host memory into the caches of n_layers layers (rows
+ * [0, L); other rows untouched) after checking its header against the running
+ * model: magic and version, model_id, dtype, n_kv_heads, head_dim, n_layers
+ * (KVR_ERR_MISMATCH on any difference), L <= capacity (KVR_ERR_CAPACITY),
+ * payload within host_bytes (KVR_ERR_WORKSPACE).  The checks run on the host
+ * before any copy; *L_out receives L (Alg. 2: the continuation starts at m.L).
+ */
+int kvr_artifact_load(const kvr_desc *desc, const char *model_id, int32_t n_layers, const void *host,
+                      size_t host_bytes, void *const *kcaches, void *const *vcaches, int64_t *L_out,
+                      void *stream);
 
 /*
  * Workspace bytes a continuation needs: n <= 1 for kvr_continue with

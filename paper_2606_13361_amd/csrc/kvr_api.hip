@@ -193,6 +193,7 @@ const char *kvr_strerror(int status) {
         case KVR_ERR_WORKSPACE: return "workspace smaller than kvr_workspace_bytes()";
         case KVR_ERR_ALIGN: return "device pointer not 16-byte aligned";
         case KVR_ERR_DEVICE: return "HIP call or kernel launch failed";
+        case KVR_ERR_MISMATCH: return "artifact metadata does not match the running model (model id, dtype or shape)";
         default: return "unknown kvr status";
     }
 }

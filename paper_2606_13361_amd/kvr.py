@@ -17,11 +17,14 @@ LIB_PATH = os.path.join(_PKG, "libkvr.so")
 
 KVR_OK, KVR_ERR_NULL, KVR_ERR_SHAPE, KVR_ERR_DTYPE = 0, 1, 2, 3
 KVR_ERR_CAPACITY, KVR_ERR_WORKSPACE, KVR_ERR_ALIGN, KVR_ERR_DEVICE = 4, 5, 6, 7
+KVR_ERR_MISMATCH = 8
+KVR_ARTIFACT_HEADER_BYTES = 256
 KVR_BF16, KVR_F32 = 0, 1
 
 EXPORTS = ("kvr_prefill", "kvr_continue", "kvr_continue_batched", "kvr_cache_append",
            "kvr_workspace_bytes", "kvr_strerror", "kvr_abi_version",
-           "kvr_q8_bytes", "kvr_quantize_cache", "kvr_continue_q8")
+           "kvr_q8_bytes", "kvr_quantize_cache", "kvr_continue_q8",
+           "kvr_artifact_bytes", "kvr_artifact_save", "kvr_artifact_load")
 
 _TORCH_DTYPE = {KVR_BF16: torch.bfloat16, KVR_F32: torch.float32}
 
@@ -64,11 +67,18 @@ def load():
     lib.kvr_q8_bytes.restype = SZ
     lib.kvr_quantize_cache.argtypes = [D, P, P, I64, P, P, P, P]
     lib.kvr_continue_q8.argtypes = [D, P, P, P, P, P, P, I64, I64, P, P, SZ, P]
+    PP = ctypes.POINTER(ctypes.c_void_p)
+    lib.kvr_artifact_bytes.argtypes = [D, ctypes.c_int32, I64]
+    lib.kvr_artifact_bytes.restype = SZ
+    lib.kvr_artifact_save.argtypes = [D, ctypes.c_char_p, ctypes.c_int32, I64, PP, PP, P, SZ, P]
+    lib.kvr_artifact_load.argtypes = [D, ctypes.c_char_p, ctypes.c_int32, P, SZ, PP, PP,
+                                      ctypes.POINTER(ctypes.c_int64), P]
     lib.kvr_strerror.argtypes = [ctypes.c_int]
     lib.kvr_strerror.restype = ctypes.c_char_p
     lib.kvr_abi_version.argtypes = []
     for f in (lib.kvr_prefill, lib.kvr_continue, lib.kvr_continue_batched, lib.kvr_cache_append,
-              lib.kvr_abi_version, lib.kvr_quantize_cache, lib.kvr_continue_q8):
+              lib.kvr_abi_version, lib.kvr_quantize_cache, lib.kvr_continue_q8, lib.kvr_artifact_save,
+              lib.kvr_artifact_load):
         f.restype = ctypes.c_int
     _lib = lib
     return lib
@@ -226,6 +236,50 @@ def kvr_continue_q8(desc, Qs, Ks, Vs, kq, vq, scales, L_prefix, S, out, ws=None,
     wp, wn = _workspace(ws)
     _raise(load().kvr_continue_q8(ctypes.byref(desc), q, k, v, a, b, sc, int(L_prefix), int(S), o, wp, wn,
                                   _stream(stream)), "kvr_continue_q8")
+
+
+def kvr_artifact_bytes(desc, n_layers, L):
+    nb = load().kvr_artifact_bytes(ctypes.byref(desc), int(n_layers), int(L))
+    if nb == ctypes.c_size_t(-1).value:
+        raise ValueError("invalid descriptor, layer count or length")
+    return nb
+
+
+def _host_buffer(host, name):
+    if not isinstance(host, torch.Tensor) or host.is_cuda or host.dtype != torch.uint8 or not host.is_contiguous():
+        raise ValueError("%s must be a contiguous uint8 CPU tensor (pinned for asynchronous copies)" % name)
+    return host.data_ptr(), host.numel()
+
+
+def _layer_ptrs(desc, caches, name):
+    arr = (ctypes.c_void_p * len(caches))()
+    shape = (desc.n_kv_heads, desc.capacity, desc.head_dim)
+    for i, c in enumerate(caches):
+        arr[i] = _check(c, "%s[%d]" % (name, i), desc, shape)
+    return arr
+
+
+def kvr_artifact_save(desc, model_id, kcaches, vcaches, L, host, stream=None):
+    """Serialize rows [0, L) of every layer's caches into the host tensor (Alg. 1)."""
+    if len(kcaches) != len(vcaches) or not kcaches:
+        raise ValueError("one K and one V cache per layer")
+    hp, hn = _host_buffer(host, "host")
+    _raise(load().kvr_artifact_save(ctypes.byref(desc), model_id.encode(), len(kcaches), int(L),
+                                    _layer_ptrs(desc, kcaches, "kcaches"), _layer_ptrs(desc, vcaches, "vcaches"),
+                                    hp, hn, _stream(stream)), "kvr_artifact_save")
+
+
+def kvr_artifact_load(desc, model_id, host, kcaches, vcaches, stream=None):
+    """Check the artifact's metadata against (model_id, desc, layer count) and load it
+    into the caches (Alg. 2); returns L, where the continuation starts."""
+    if len(kcaches) != len(vcaches) or not kcaches:
+        raise ValueError("one K and one V cache per layer")
+    hp, hn = _host_buffer(host, "host")
+    L = ctypes.c_int64(-1)
+    _raise(load().kvr_artifact_load(ctypes.byref(desc), model_id.encode(), len(kcaches), hp, hn,
+                                    _layer_ptrs(desc, kcaches, "kcaches"), _layer_ptrs(desc, vcaches, "vcaches"),
+                                    ctypes.byref(L), _stream(stream)), "kvr_artifact_load")
+    return L.value
 
 
 def _workspace(ws):
