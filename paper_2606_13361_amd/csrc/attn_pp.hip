@@ -24,6 +24,8 @@
 // The workgroup holding the first query row of a token also copies that
 // token's K/V rows into the cache, from the tiles still in LDS after its
 // attention work; output rows leave through LDS as full 256-byte rows.
+#include <type_traits>
+
 #include "attn_common.hpp"
 
 namespace kvr {
@@ -43,9 +45,18 @@ static_assert(kSlackSum == (float)(1 << (int)kRescaleSlack), "slack sum must mat
 
 __device__ __forceinline__ int swz(int row) { return ((row >> 2) & 3) | ((row & 3) << 2); }
 
+// the four loads of a step: K and V bases (uniform), the lanes' offsets for row
+// groups 0 and 1, the LDS destination
+struct TileSrc {
+    uint64_t kb, vb;
+    uint32_t o0, o1;
+    int lds;          // LDS byte offset of load 0
+};
+
 template <int MODE>
 __global__ __launch_bounds__(PP_THREADS) void attn_pp_kernel(const AttnParams p) {
-    __shared__ __attribute__((aligned(1024))) unsigned char smem[NS * STAGE];
+    // the ring, then the scratch area that loads with nothing to move write to
+    __shared__ __attribute__((aligned(1024))) unsigned char smem[NS * STAGE + TILE + 2048];
 
     const int tid = threadIdx.x;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform: scalar branches
@@ -99,37 +110,66 @@ __global__ __launch_bounds__(PP_THREADS) void attn_pp_kernel(const AttnParams p)
     const uint64_t kc_a = (uint64_t)(uintptr_t)p.kc + (uint64_t)g * p.cap * ROWB;
     const uint64_t vc_a = (uint64_t)(uintptr_t)p.vc + (uint64_t)g * p.cap * ROWB;
     int lrow[2];
-    uint32_t lchunk[2], off_n[2], off_c[2];
+    uint32_t lchunk[2];
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
         lrow[i] = 8 * wave + 4 * i + (lane >> 4);
         lchunk[i] = 16u * (uint32_t)((lane & 15) ^ swz(lrow[i]));
-        off_n[i] = (uint32_t)(lrow[i] * nstride_b) + lchunk[i];
-        off_c[i] = (uint32_t)(lrow[i] * ROWB) + lchunk[i];
     }
-    // load q (0..3) of this wave's four for tile t: K row groups 0, 1, then V row groups 0, 1
-    auto dma_part = [=](int t, int q) {
+    // A tile whose 64 rows are all cached or all new is "fast": its loads are
+    // the saddr form (one uniform base per tensor, a per-lane row offset),
+    // issued from inside a step as straight-line code.  Any other tile (the
+    // prefix/new boundary, the ragged end) is loaded row by row, before the step.
+    auto tile_fast = [&](int t) {
         const int k0 = t * KEYS;
-        const int i = q & 1;
-        const unsigned char *dst = smem + (t % NS) * STAGE + 8 * wave * ROWB + (q >> 1) * TILE + 1024 * i;
-        const uint64_t nbase = (q >> 1) ? vn_a : kn_a;
-        const uint64_t cbase = (q >> 1) ? vc_a : kc_a;
-        if (k0 + KEYS <= npre) {                               // all rows cached
-            dma16_s(cbase + (uint64_t)k0 * ROWB, off_c[i], dst);
-        } else if (k0 >= npre && k0 + KEYS <= ke) {            // all rows new
-            dma16_s(nbase + (uint64_t)(k0 - npre) * nstride_b, off_n[i], dst);
-        } else {
-            // prefix/new boundary or ragged end: per-row source, rows past ke repeat
-            // row ke-1 (beyond every causal bound, masked)
-            const int key = min(k0 + lrow[i], ke - 1);
-            const uint64_t off = key < npre ? (uint64_t)key * ROWB : (uint64_t)(key - npre) * (uint64_t)nstride_b;
-            const uint64_t sel = 0 - (uint64_t)(key < npre);   // base select by mask
-            dma16((const void *)(((cbase & sel) | (nbase & ~sel)) + off + lchunk[i]), dst);
+        return k0 + KEYS <= npre || (k0 >= npre && k0 + KEYS <= ke);
+    };
+    auto load_rows = [&](int t) {
+        // per-row source; rows past ke repeat row ke-1 (beyond every causal
+        // bound, masked)
+        const int lds0 = (t % NS) * STAGE + 8 * wave * ROWB;
+#pragma unroll
+        for (int q = 0; q < PP_LOADS; ++q) {
+            const int i = q & 1;
+            const uint64_t nbase = (q >> 1) ? vn_a : kn_a;
+            const uint64_t cbase = (q >> 1) ? vc_a : kc_a;
+            const int key = min(t * KEYS + lrow[i], ke - 1);
+            const bool c = key < npre;
+            const uint64_t off = (uint64_t)(c ? key : key - npre) * (c ? (uint64_t)ROWB : (uint64_t)nstride_b);
+            const uint64_t sel = 0 - (uint64_t)c;               // base select by mask
+            dma16((const void *)(((cbase & sel) | (nbase & ~sel)) + off + lchunk[i]),
+                  smem + lds0 + (q >> 1) * TILE + 1024 * i);
         }
     };
-    auto load_tile = [=](int t) {
+    // The four loads a step issues (load q: K row groups 0, 1, then V row groups
+    // 0, 1).  For a fast tile dt they are its loads; otherwise (no tile left, or
+    // a tile loaded row by row just before) the same four instructions re-read
+    // the first 256 bytes of the keys into a scratch area of LDS that nothing
+    // reads, so every step's loads are branch-free and the wait counts never
+    // change.  Every choice here is wave-uniform.
+    auto plan = [&](int dt) {
+        const bool fast = dt >= 0 && tile_fast(dt);
+        if (dt >= 0 && !fast) load_rows(dt);
+        const int k0 = dt * KEYS;
+        const bool cached = k0 + KEYS <= npre;
+        const uint64_t nrow = (uint64_t)(k0 - npre) * nstride_b;
+        const uint64_t row0_k = npre > 0 ? kc_a : kn_a;
+        TileSrc f;
+        f.kb = fast ? (cached ? kc_a + (uint64_t)k0 * ROWB : kn_a + nrow) : row0_k;
+        f.vb = fast ? (cached ? vc_a + (uint64_t)k0 * ROWB : vn_a + nrow) : row0_k;
+        const uint32_t stride = fast ? (cached ? (uint32_t)ROWB : (uint32_t)nstride_b) : 0u;
+        f.o0 = (uint32_t)lrow[0] * stride + lchunk[0];
+        f.o1 = (uint32_t)lrow[1] * stride + lchunk[1];
+        f.lds = fast ? (dt % NS) * STAGE + 8 * wave * ROWB : NS * STAGE;
+        return f;
+    };
+    auto dma_fast = [&](const TileSrc &f, int q) {
+        dma16_s((q >> 1) ? f.vb : f.kb, (q & 1) ? f.o1 : f.o0, smem + f.lds + (q >> 1) * TILE + 1024 * (q & 1));
+    };
+    auto load_tile = [&](int t) {
+        const TileSrc f = plan(t);
 #pragma unroll
-        for (int q = 0; q < PP_LOADS; ++q) dma_part(t, q);
+        for (int q = 0; q < PP_LOADS; ++q) dma_fast(f, q);
     };
 
     // ---- read maps (per lane, loop invariant); as in the streamed kernel
@@ -201,7 +241,8 @@ __global__ __launch_bounds__(PP_THREADS) void attn_pp_kernel(const AttnParams p)
 #pragma unroll
         for (int idx = 0; idx < 16; ++idx) pv(vfrag(vs_, idx), idx);
     };
-    auto gemm = [&](int t, int dt) {      // both; issues the loads of tile dt (if >= 0) between chunks
+    auto gemm = [&](auto with_loads, int t, const TileSrc &f) {   // both; with_loads: the
+                                                                   // step's loads between chunks
         const unsigned char *ks_ = smem + (t % NS) * STAGE;
         const unsigned char *vs_ = smem + ((t + NS - 1) % NS) * STAGE + TILE;
         s_zero();
@@ -219,7 +260,9 @@ __global__ __launch_bounds__(PP_THREADS) void attn_pp_kernel(const AttnParams p)
             pv(v0, 2 * c);
             sm(k1, 1, c);
             pv(v1, 2 * c + 1);
-            if ((c & 1) && dt >= 0) dma_part(dt, c >> 1);
+            if constexpr (decltype(with_loads)::value) {
+                if (c & 1) dma_fast(f, c >> 1);
+            }
             __builtin_amdgcn_sched_barrier(0);
             if (c + 1 < 8) {
                 k0 = nk0; k1 = nk1; v0 = nv0; v1 = nv1;
@@ -227,7 +270,8 @@ __global__ __launch_bounds__(PP_THREADS) void attn_pp_kernel(const AttnParams p)
         }
     };
     // SOFT(t): causal mask, row max, lazy rescale of (O, l), P_t = 2^(S c2 - m)
-    auto soft = [&](int t, int dt) {      // issues the loads of tile dt (if >= 0) among the exps
+    auto soft = [&](auto with_loads, int t, const TileSrc &f) {   // with_loads: the step's
+                                                                   // loads among the exps
         const int k0 = t * KEYS;
         if (k0 + KEYS > k_full) {
             const int lim = max(-1, min(pos - k0, KEYS));
@@ -243,7 +287,7 @@ __global__ __launch_bounds__(PP_THREADS) void attn_pp_kernel(const AttnParams p)
         // only when some lane's weights sum above 2^kRescaleSlack (then one of
         // them may exceed it) -- the first tile (m = -1e30) always, later tiles
         // almost never
-        auto exps = [&](int dtl) {
+        auto exps = [&](auto loads) {
             float lsum[4] = {0.f, 0.f, 0.f, 0.f};   // four independent partial sums
 #pragma unroll
             for (int st = 0; st < 2; ++st)
@@ -252,14 +296,18 @@ __global__ __launch_bounds__(PP_THREADS) void attn_pp_kernel(const AttnParams p)
                     const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[st][i], c2, -rs.m));
                     const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[st][i + 1], c2, -rs.m));
                     const uint32_t pk = pack_bf16x2(p0, p1);
+                    // row sums with plain fp32 adds: a v_dot2 would queue behind the
+                    // other wave's MFMAs on the matrix pipe and stall this wave
                     float &acc = lsum[(i >> 1) & 3];
-                    acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, pk), kOnes, acc, false);
+                    acc += p0 + p1;
                     pf[st][i >> 3][(i & 7) >> 1] = pk;
-                    if ((i & 7) == 6 && dtl >= 0) dma_part(dtl, 2 * st + (i >> 3));
+                    if constexpr (decltype(loads)::value) {
+                        if ((i & 7) == 6) dma_fast(f, 2 * st + (i >> 3));
+                    }
                 }
             return (lsum[0] + lsum[1]) + (lsum[2] + lsum[3]);
         };
-        float part = exps(dt);
+        float part = exps(with_loads);
         if (__ballot(!(part <= kSlackSum))) {
             // row max as a tree (5 dependent levels)
             float v[32];
@@ -283,7 +331,7 @@ __global__ __launch_bounds__(PP_THREADS) void attn_pp_kernel(const AttnParams p)
                 for (int mt = 0; mt < D / 32; ++mt)
 #pragma unroll
                     for (int i = 0; i < 16; ++i) rs.o[mt][i] *= alpha;
-                part = exps(-1);
+                part = exps(std::false_type{});
             }
         }
         rs.l += part;
@@ -317,18 +365,20 @@ __global__ __launch_bounds__(PP_THREADS) void attn_pp_kernel(const AttnParams p)
         if (act) { __builtin_amdgcn_s_setprio(1); gemm_s(0); __builtin_amdgcn_s_setprio(0); }
         if (next(0) >= 0) load_tile(next(0));
         sync(1);
-        if (act) soft(0, -1);
+        if (act) soft(std::false_type{}, 0, TileSrc{});
         for (int t = 1; t < ntiles; ++t) {
             sync(2 * t);
+            const TileSrc f = plan(next(t));
             if (act) {
                 __builtin_amdgcn_s_setprio(1);
-                gemm(t, next(t));
+                gemm(std::true_type{}, t, f);
                 __builtin_amdgcn_s_setprio(0);
-            } else if (next(t) >= 0) {
-                load_tile(next(t));
+            } else {
+#pragma unroll
+                for (int q = 0; q < PP_LOADS; ++q) dma_fast(f, q);
             }
             sync(2 * t + 1);
-            if (act) soft(t, -1);
+            if (act) soft(std::false_type{}, t, TileSrc{});
         }
         sync(2 * ntiles);
         if (act) { __builtin_amdgcn_s_setprio(1); gemm_pv(ntiles); __builtin_amdgcn_s_setprio(0); }
@@ -340,17 +390,22 @@ __global__ __launch_bounds__(PP_THREADS) void attn_pp_kernel(const AttnParams p)
         if (act) { __builtin_amdgcn_s_setprio(1); gemm_s(0); __builtin_amdgcn_s_setprio(0); }
         for (int t = 1; t < ntiles; ++t) {
             sync(2 * t);
-            if (act) soft(t - 1, next(t));
-            else if (next(t) >= 0) load_tile(next(t));
+            const TileSrc f = plan(next(t));
+            if (act) {
+                soft(std::true_type{}, t - 1, f);
+            } else {
+#pragma unroll
+                for (int q = 0; q < PP_LOADS; ++q) dma_fast(f, q);
+            }
             sync(2 * t + 1);
             if (act) {
                 __builtin_amdgcn_s_setprio(1);
-                gemm(t, -1);
+                gemm(std::false_type{}, t, TileSrc{});
                 __builtin_amdgcn_s_setprio(0);
             }
         }
         sync(2 * ntiles);
-        if (act) soft(ntiles - 1, -1);
+        if (act) soft(std::false_type{}, ntiles - 1, TileSrc{});
         sync(2 * ntiles + 1);
         if (act) { __builtin_amdgcn_s_setprio(1); gemm_pv(ntiles); __builtin_amdgcn_s_setprio(0); }
     }
