@@ -148,6 +148,24 @@ __device__ __forceinline__ void dma16_s(uint64_t base, uint32_t off, const void 
     asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2" ::"s"(lds), "v"(off), "s"(base) : "m0");
 }
 
+// dma16_s for one instruction under the exec mask when `on` is nonzero, and
+// with no lane enabled (nothing loaded, nothing written) when it is zero; `on`
+// must be wave-uniform.  exec is restored inside the statement.
+__device__ __forceinline__ void dma16_s_if(uint64_t base, uint32_t off, const void *lds_dst, int on) {
+    const uint32_t lds = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void *)lds_dst;
+    const int on_s = __builtin_amdgcn_readfirstlane(on);
+    uint64_t saved, m;
+    asm volatile("s_mov_b32 m0, %2\n\t"
+                 "s_cmp_lg_u32 %5, 0\n\t"
+                 "s_cselect_b64 %1, -1, 0\n\t"
+                 "s_and_saveexec_b64 %0, %1\n\t"
+                 "global_load_lds_dwordx4 %3, %4\n\t"
+                 "s_mov_b64 exec, %0"
+                 : "=&s"(saved), "=&s"(m)
+                 : "s"(lds), "v"(off), "s"(base), "s"(on_s)
+                 : "m0", "scc");
+}
+
 // 16-byte load through a buffer resource: the 64-bit base lives in SGPRs
 // (one per tile, built with scalar arithmetic) and each lane supplies a
 // 32-bit byte offset, so interior tiles need no per-lane address arithmetic.

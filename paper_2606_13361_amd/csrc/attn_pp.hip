@@ -51,12 +51,12 @@ struct TileSrc {
     uint64_t kb, vb;
     uint32_t o0, o1;
     int lds;          // LDS byte offset of load 0
+    int on;           // 1: the loads run; 0: they run with no lane enabled
 };
 
 template <int MODE>
 __global__ __launch_bounds__(PP_THREADS) void attn_pp_kernel(const AttnParams p) {
-    // the ring, then the scratch area that loads with nothing to move write to
-    __shared__ __attribute__((aligned(1024))) unsigned char smem[NS * STAGE + TILE + 2048];
+    __shared__ __attribute__((aligned(1024))) unsigned char smem[NS * STAGE];
 
     const int tid = threadIdx.x;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform: scalar branches
@@ -143,10 +143,9 @@ __global__ __launch_bounds__(PP_THREADS) void attn_pp_kernel(const AttnParams p)
     };
     // The four loads a step issues (load q: K row groups 0, 1, then V row groups
     // 0, 1).  For a fast tile dt they are its loads; otherwise (no tile left, or
-    // a tile loaded row by row just before) the same four instructions re-read
-    // the first 256 bytes of the keys into a scratch area of LDS that nothing
-    // reads, so every step's loads are branch-free and the wait counts never
-    // change.  Every choice here is wave-uniform.
+    // a tile loaded row by row just before) the same four instructions run with
+    // no lane enabled, so every step's loads are branch-free.  Every choice here
+    // is wave-uniform.
     auto plan = [&](int dt) {
         const bool fast = dt >= 0 && tile_fast(dt);
         if (dt >= 0 && !fast) load_rows(dt);
@@ -160,11 +159,12 @@ __global__ __launch_bounds__(PP_THREADS) void attn_pp_kernel(const AttnParams p)
         const uint32_t stride = fast ? (cached ? (uint32_t)ROWB : (uint32_t)nstride_b) : 0u;
         f.o0 = (uint32_t)lrow[0] * stride + lchunk[0];
         f.o1 = (uint32_t)lrow[1] * stride + lchunk[1];
-        f.lds = fast ? (dt % NS) * STAGE + 8 * wave * ROWB : NS * STAGE;
+        f.lds = fast ? (dt % NS) * STAGE + 8 * wave * ROWB : 0;
+        f.on = fast ? 1 : 0;
         return f;
     };
     auto dma_fast = [&](const TileSrc &f, int q) {
-        dma16_s((q >> 1) ? f.vb : f.kb, (q & 1) ? f.o1 : f.o0, smem + f.lds + (q >> 1) * TILE + 1024 * (q & 1));
+        dma16_s_if((q >> 1) ? f.vb : f.kb, (q & 1) ? f.o1 : f.o0, smem + f.lds + (q >> 1) * TILE + 1024 * (q & 1), f.on);
     };
     auto load_tile = [&](int t) {
         const TileSrc f = plan(t);
@@ -358,6 +358,13 @@ __global__ __launch_bounds__(PP_THREADS) void attn_pp_kernel(const AttnParams p)
     };
     load_tile(0);
     if (ntiles > 1) load_tile(1);
+    // One use of the Q fragments here, on every path: the compiler puts its wait
+    // for their loads (which also covers tiles 0 and 1, issued after them) at
+    // this point, and none in the loops below -- otherwise a path that reaches
+    // a loop without having used them makes it wait for every load in flight at
+    // the first product of each step.
+#pragma unroll
+    for (int ks = 0; ks < D / 16; ++ks) asm volatile("" ::"v"(qf[ks]));
     const bool act = wave_active;
     auto next = [&](int t) { return t + 2 < ntiles ? t + 2 : -1; };   // tile issued in phase 2t
     if (gw == 0) {
