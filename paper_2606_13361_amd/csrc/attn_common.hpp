@@ -126,8 +126,6 @@ struct RowState {
     }
 };
 
-__device__ const bf16x2 kOnes = {(__bf16)1.0f, (__bf16)1.0f};
-
 // Direct-to-LDS load of 16 bytes per lane: lane l's bytes land at LDS byte
 // lds + 16*l (lds is wave-uniform).  Issued as inline asm so the compiler does
 // not treat it as an LDS write it must wait for before every later LDS read
@@ -256,9 +254,8 @@ __device__ __forceinline__ void tile_step(RowState<D> &rs, const u32x4 (&qf)[D /
             const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[st][i], c2, -rs.m));
             const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[st][i + 1], c2, -rs.m));
             const uint32_t pk = pack_bf16x2(p0, p1);
-            // normalise by the weights the PV product really uses (bf16-rounded):
-            // the output is an exact convex combination of V rows
-            lsum = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, pk), kOnes, lsum, false);
+            // row sum in fp32 adds (a v_dot2 would wait behind MFMAs on the matrix pipe)
+            lsum += p0 + p1;
             pf[st][i >> 3][(i & 7) >> 1] = pk;
         }
     }

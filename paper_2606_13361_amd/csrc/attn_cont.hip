@@ -427,7 +427,7 @@ __global__ __launch_bounds__(THREADS) void attn_cont_kernel(const AttnParams p) 
                 const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[c][i], c2s, -rs[c].m));
                 const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[c][i + 1], c2s, -rs[c].m));
                 const uint32_t pk = pack_bf16x2(p0, p1);
-                lsum = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, pk), kOnes, lsum, false);
+                lsum += p0 + p1;
                 pf[c][i >> 3][(i & 7) >> 1] = pk;
             }
             rs[c].l += lsum;
