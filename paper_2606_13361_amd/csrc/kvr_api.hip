@@ -147,12 +147,12 @@ int launch_single(const kvr_desc *d, int mode, const void *Q, const void *K, con
     if (grid > 0x7fffffff) return KVR_ERR_SHAPE;
     hipError_t e;
     if (mode == kModeContinue && use_cont(d, n_tok)) {
-        if (qscale) {
-            const int nct = (int)((rows + 31) / 32);
-            e = launch_attn_cont(p, nct, true, (int)grid, stream);
-        } else {
-            e = launch_attn_rows(p, (int)grid, stream);
-        }
+        // up to 32 rows (decode steps): the waves split the keys, one column
+        // tile each; more rows: the waves split the rows (no in-workgroup
+        // merge); the int8 artifact: the waves split the keys
+        const int nct = (int)((rows + 31) / 32);
+        if (qscale || nct == 1) e = launch_attn_cont(p, nct, qscale != nullptr, (int)grid, stream);
+        else e = launch_attn_rows(p, (int)grid, stream);
     } else if (mode == kModePrefill && use_pp(d)) {
         const int64_t pp_tiles = (rows + kRowsPP - 1) / kRowsPP;
         p.tiles_total = (int32_t)pp_tiles;

@@ -76,11 +76,11 @@ hipError_t launch_merge_bf16(const MergeParams &p, int head_dim, hipStream_t s);
 // matrix and softmax steps
 constexpr int kRowsPP = 256;   // query rows per workgroup (8 waves x 32)
 hipError_t launch_attn_pp(const AttnParams &p, int mode, int grid, hipStream_t s);
-// bf16 continuation for G*S <= 96 rows (D = 128): the waves of a workgroup
-// split the rows and share one ring of key stages
+// bf16 continuation for G*S <= 96 rows (D = 128).  33..96 rows: the waves of
+// a workgroup split the rows and share one ring of key stages; up to 32 rows
+// (decode steps) and the int8 artifact: the waves split the keys
 constexpr int kContMaxRows = 96;
 hipError_t launch_attn_rows(const AttnParams &p, int grid, hipStream_t s);
-// the same over the int8 artifact: the waves split the keys
 hipError_t launch_attn_cont(const AttnParams &p, int ncol_tiles, bool q8, int grid, hipStream_t s);
 // int8 artifact
 hipError_t launch_quantize(const QuantParams &p, hipStream_t s);

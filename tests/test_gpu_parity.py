@@ -146,6 +146,26 @@ def test_continue_bf16_vs_oracle_and_prefill(Lp, S):
     assert maxabs(cont, want) <= TOL[torch.bfloat16]
 
 
+@pytest.mark.parametrize("Hq,Hkv,Lp,S", [
+    (8, 8, 900, 50), (16, 8, 2000, 40), (64, 8, 1500, 9), (32, 8, 513, 10), (32, 8, 4159, 12), (8, 8, 70, 96),
+])
+def test_continue_group_sizes(Hq, Hkv, Lp, S):
+    """Other GQA groups and row counts (33..96 rows per kv head, one or several
+    column tiles per wave group, ragged prefixes): oracle and Claim 1."""
+    say("continue bf16 %d/%d/128 Lp=%d S=%d" % (Hq, Hkv, Lp, S))
+    sh = W.Shape(Hq, Hkv, 128, torch.bfloat16)
+    n = Lp + S
+    q, k, v = W.qkv(n, sh, seed=5 + Hq + Lp)
+    full, _, _, _ = gpu_prefill(sh, q, k, v)
+    _, kc, vc, d = gpu_prefill(sh, q[:Lp], k[:Lp], v[:Lp], capacity=n + 1)
+    cont = gpu_continue(d, q[Lp:], k[Lp:], v[Lp:], kc, vc, Lp)
+    torch.cuda.synchronize()
+    claim1(cont, full[Lp:])
+    want, _ = ref.continue_(q[Lp:], k[Lp:], v[Lp:], k[:Lp].transpose(0, 1).contiguous(),
+                            v[:Lp].transpose(0, 1).contiguous(), Lp)
+    assert maxabs(cont, want) <= TOL[torch.bfloat16]
+
+
 @pytest.mark.parametrize("Lp,S", [(0, 5), (129, 16), (600, 33)])
 def test_continue_fp32_vs_oracle(Lp, S):
     say("continue fp32 8/2/64 Lp=%d S=%d" % (Lp, S))
