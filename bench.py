@@ -213,7 +213,7 @@ def main():
         "prefill": {"kernel": "attn_pp_kernel<prefill>", "bound": "mfma", "achieved": round(pf_tflops, 2),
                     "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(pf_tflops / PEAK_BF16_TFLOPS, 4),
                     "work_per_launch": pf_flops, "avg_launch_ms": round(avg["prefill"] * 1e3, 4)},
-        "continue": {"kernel": "attn_cont_kernel<3> + merge_bf16_kernel<128>", "bound": "hbm",
+        "continue": {"kernel": "attn_rows_kernel + merge_bf16_kernel<128>", "bound": "hbm",
                      "achieved": round(c_gbps, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
                      "frac": round(c_gbps / PEAK_HBM_GBPS, 4), "work_per_launch": c_bytes,
                      "avg_launch_ms": round(avg["continue"] * 1e3, 4)},
