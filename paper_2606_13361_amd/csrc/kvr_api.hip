@@ -19,6 +19,8 @@ constexpr int64_t kMaxKeys = (int64_t)1 << 40;
 constexpr int64_t kTargetWorkgroupsStaged = 512;
 constexpr int64_t kTargetWorkgroupsCont = 256;   // split-K-in-workgroup kernel: one per CU (155 KB of LDS)
 constexpr int64_t kMinSplitKeys = 256;
+// longest key range per workgroup for which the row-split continuation is used
+constexpr int64_t kRowsSplitMaxKeys = 640;
 
 // Continuations of at most kContMaxRows query rows per kv head (decode steps,
 // short suffixes) at bf16 / head_dim 128 use the kernel whose waves split the keys.
@@ -147,12 +149,18 @@ int launch_single(const kvr_desc *d, int mode, const void *Q, const void *K, con
     if (grid > 0x7fffffff) return KVR_ERR_SHAPE;
     hipError_t e;
     if (mode == kModeContinue && use_cont(d, n_tok)) {
-        // up to 32 rows (decode steps): the waves split the keys, one column
-        // tile each; more rows: the waves split the rows (no in-workgroup
-        // merge); the int8 artifact: the waves split the keys
+        // The row split removes the in-workgroup merge and the suffix stage
+        // that one wave alone would run, but spends about a third more matrix
+        // and softmax work per key (24 of 32 MFMA columns, every wave on every
+        // stage): it pays for short key ranges per workgroup and more than 32
+        // rows.  Decode steps (one column tile), long ranges and the int8
+        // artifact use the kernel whose waves split the keys.
         const int nct = (int)((rows + 31) / 32);
-        if (qscale || nct == 1) e = launch_attn_cont(p, nct, qscale != nullptr, (int)grid, stream);
-        else e = launch_attn_rows(p, (int)grid, stream);
+        const int64_t keys_per_wg = p.nsplit > 1 ? p.chunk : n_prefix + n_tok;
+        if (qscale || nct == 1 || keys_per_wg > kRowsSplitMaxKeys)
+            e = launch_attn_cont(p, nct, qscale != nullptr, (int)grid, stream);
+        else
+            e = launch_attn_rows(p, (int)grid, stream);
     } else if (mode == kModePrefill && use_pp(d)) {
         const int64_t pp_tiles = (rows + kRowsPP - 1) / kRowsPP;
         p.tiles_total = (int32_t)pp_tiles;
