@@ -37,8 +37,8 @@ ELT = 2
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=50)
     ap.add_argument("--no-sweep", action="store_true")
     ap.add_argument("--no-decode36", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -318,9 +318,16 @@ def sweep(torch, kvr, A, W, dev, stream, lengths, suffix=None):
         out = torch.empty_like(q)
         kc = torch.empty((Hkv, n, D), dtype=torch.bfloat16, device=dev)
         vc = torch.empty_like(kc)
-        reps = 3 if L >= 16384 else 10
-        for _ in range(2):
+        reps = 5 if L >= 16384 else 20
+        # warm up for at least 0.2 s of back-to-back calls: the engine clock
+        # ramps over milliseconds under a sustained MFMA load, and a 2-8 ms
+        # kernel timed right after two calls would be measured mid-ramp
+        t_w = time.perf_counter()
+        while True:
             kvr.kvr_prefill(desc, q, k, v, n, out, kc, vc)
+            torch.cuda.synchronize()
+            if time.perf_counter() - t_w >= 0.2:
+                break
         tp = timed(torch, stream, lambda i: kvr.kvr_prefill(desc, q, k, v, n, out, kc, vc), reps)
         # continuation over R distinct caches (>= 1 GiB in total)
         cache_bytes = 2 * Hkv * n * D * 2
