@@ -28,9 +28,10 @@
  *         Q, out            [tokens][n_q_heads][head_dim]
  *         K, V (new rows)   [tokens][n_kv_heads][head_dim]
  *         kcache, vcache    [n_kv_heads][capacity][head_dim]
- *     Elements are bf16 (KVR_BF16) or fp32 (KVR_F32) as the descriptor says;
- *     bf16 inputs accumulate in fp32 and the bf16 output is rounded to
- *     nearest-even.
+ *     Elements are bf16 (KVR_BF16), fp16 (KVR_F16, the paper's precision) or
+ *     fp32 (KVR_F32) as the descriptor says; 16-bit inputs accumulate in fp32,
+ *     the attention weights enter the second product in the input format, and
+ *     16-bit outputs are rounded to nearest-even.
  *   - Every call validates all arguments on the host, synchronously, before
  *     any HIP call; on an error nothing is launched and a kvr_status != 0 is
  *     returned.  On success the work is enqueued on `stream` (a hipStream_t;
@@ -65,7 +66,7 @@ typedef enum {
                               heads, head_dim, layers) or its header is not valid  */
 } kvr_status;
 
-typedef enum { KVR_BF16 = 0, KVR_F32 = 1 } kvr_dtype;
+typedef enum { KVR_BF16 = 0, KVR_F32 = 1, KVR_F16 = 2 } kvr_dtype;
 
 /*
  * Layer descriptor.  The paper's artifact metadata (model id, dtype, length;

@@ -34,14 +34,14 @@ static_assert(sizeof(ArtifactHeader) == KVR_ARTIFACT_HEADER_BYTES, "artifact hea
 
 int valid_desc(const kvr_desc *d) {
     if (!d) return KVR_ERR_NULL;
-    if (d->dtype != KVR_BF16 && d->dtype != KVR_F32) return KVR_ERR_DTYPE;
+    if (d->dtype != KVR_BF16 && d->dtype != KVR_F32 && d->dtype != KVR_F16) return KVR_ERR_DTYPE;
     if (d->n_q_heads <= 0 || d->n_kv_heads <= 0 || d->n_q_heads % d->n_kv_heads != 0) return KVR_ERR_SHAPE;
     if (d->head_dim != 64 && d->head_dim != 128) return KVR_ERR_SHAPE;
     if (d->capacity < 0 || d->reserved != 0) return KVR_ERR_SHAPE;
     return KVR_OK;
 }
 
-size_t elt(const kvr_desc *d) { return d->dtype == KVR_BF16 ? 2 : 4; }
+size_t elt(const kvr_desc *d) { return d->dtype == KVR_F32 ? 4 : 2; }
 
 // bytes of one layer's K (or V) rows [0, L)
 size_t tensor_bytes(const kvr_desc *d, int64_t L) { return (size_t)d->n_kv_heads * (size_t)L * d->head_dim * elt(d); }

@@ -36,7 +36,7 @@ struct Tile {
     static_assert(KPT * RPP == BN, "tile staging must cover the tile");
 };
 
-template <int D, int MODE>
+template <int D, int MODE, class E>
 __global__ __launch_bounds__(THREADS) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void attn_bf16_kernel(const AttnParams p) {
     using T = Tile<D>;
@@ -69,7 +69,7 @@ void attn_bf16_kernel(const AttnParams p) {
     // ---- Q^T fragments (MFMA B operand): column j, head-dim slots 16*ks + 8*grp + 0..7
     u32x4 qf[D / 16];
     {
-        const __bf16 *qrow = (const __bf16 *)p.q + ((int64_t)(tok0 + tok) * p.n_q_heads + head) * D;
+        const uint16_t *qrow = (const uint16_t *)p.q + ((int64_t)(tok0 + tok) * p.n_q_heads + head) * D;
 #pragma unroll
         for (int ks = 0; ks < D / 16; ++ks)
             qf[ks] = valid ? *(const u32x4 *)(qrow + 16 * ks + 8 * grp) : (u32x4){0, 0, 0, 0};
@@ -78,13 +78,13 @@ void attn_bf16_kernel(const AttnParams p) {
     // ---- staging map: thread -> 16-byte chunk sc of rows srow + RPP * i
     const int sc = tid % T::CH;
     const int srow = tid / T::CH;
-    const __bf16 *kc = (const __bf16 *)p.kc + (int64_t)g * p.cap * D + 8 * sc;
-    const __bf16 *vc = (const __bf16 *)p.vc + (int64_t)g * p.cap * D + 8 * sc;
+    const uint16_t *kc = (const uint16_t *)p.kc + (int64_t)g * p.cap * D + 8 * sc;
+    const uint16_t *vc = (const uint16_t *)p.vc + (int64_t)g * p.cap * D + 8 * sc;
     const int64_t nstride = (int64_t)p.n_kv_heads * D;
-    const __bf16 *kn = (const __bf16 *)p.kn + (int64_t)tok0 * nstride + (int64_t)g * D + 8 * sc;
-    const __bf16 *vn = (const __bf16 *)p.vn + (int64_t)tok0 * nstride + (int64_t)g * D + 8 * sc;
-    __bf16 *kco = (__bf16 *)p.kc_out + (int64_t)g * p.cap * D + 8 * sc;   // prefill: cache rows out
-    __bf16 *vco = (__bf16 *)p.vc_out + (int64_t)g * p.cap * D + 8 * sc;
+    const uint16_t *kn = (const uint16_t *)p.kn + (int64_t)tok0 * nstride + (int64_t)g * D + 8 * sc;
+    const uint16_t *vn = (const uint16_t *)p.vn + (int64_t)tok0 * nstride + (int64_t)g * D + 8 * sc;
+    uint16_t *kco = (uint16_t *)p.kc_out + (int64_t)g * p.cap * D + 8 * sc;   // prefill: cache rows out
+    uint16_t *vco = (uint16_t *)p.vc_out + (int64_t)g * p.cap * D + 8 * sc;
 
     u32x4 kreg[T::KPT], vreg[T::KPT];
     // Interior tiles (all 64 rows from one source, none past ke, no cache row
@@ -134,8 +134,8 @@ void attn_bf16_kernel(const AttnParams p) {
                 const int64_t kk = key < ke ? key : ke - 1;
                 const bool in_cache = kk < npre;
                 const int64_t off = in_cache ? kk * D : (kk - npre) * nstride;
-                const __bf16 *kbase = in_cache ? kc : kn;
-                const __bf16 *vbase = in_cache ? vc : vn;
+                const uint16_t *kbase = in_cache ? kc : kn;
+                const uint16_t *vbase = in_cache ? vc : vn;
                 kreg[i] = *(const u32x4 *)(kbase + off);
                 vreg[i] = *(const u32x4 *)(vbase + off);
                 if constexpr (MODE == kModePrefill) {
@@ -189,7 +189,7 @@ void attn_bf16_kernel(const AttnParams p) {
             const bool mask = k0 + BN > k_full;
             const int64_t lim64 = pos - k0;
             const int lim = lim64 < -1 ? -1 : (lim64 > BN ? BN : (int)lim64);
-            tile_step<D>(
+            tile_step<E, D>(
                 rs, qf,
                 [&](int st, int ks) { return ks_ + k_lane + 32 * st * T::K_PITCH + 32 * ks; },
                 [&](int st, int kk, int h, int mt) {
@@ -200,20 +200,20 @@ void attn_bf16_kernel(const AttnParams p) {
         if (more) swrite(cur ^ 1);
         __syncthreads();
     }
-    epilogue<D, MODE>(p, w, rs, r, valid, tok, head, grp);
+    epilogue<E, D, MODE>(p, w, rs, r, valid, tok, head, grp);
 }
 
-template <int D>
+template <int D, class E>
 hipError_t launch_d(const AttnParams &p, int mode, int grid, hipStream_t s) {
     switch (mode) {
         case kModePrefill:
-            hipLaunchKernelGGL((attn_bf16_kernel<D, kModePrefill>), dim3(grid), dim3(THREADS), 0, s, p);
+            hipLaunchKernelGGL((attn_bf16_kernel<D, kModePrefill, E>), dim3(grid), dim3(THREADS), 0, s, p);
             break;
         case kModeContinue:
-            hipLaunchKernelGGL((attn_bf16_kernel<D, kModeContinue>), dim3(grid), dim3(THREADS), 0, s, p);
+            hipLaunchKernelGGL((attn_bf16_kernel<D, kModeContinue, E>), dim3(grid), dim3(THREADS), 0, s, p);
             break;
         default:
-            hipLaunchKernelGGL((attn_bf16_kernel<D, kModeReaders>), dim3(grid), dim3(THREADS), 0, s, p);
+            hipLaunchKernelGGL((attn_bf16_kernel<D, kModeReaders, E>), dim3(grid), dim3(THREADS), 0, s, p);
             break;
     }
     return hipGetLastError();
@@ -221,8 +221,9 @@ hipError_t launch_d(const AttnParams &p, int mode, int grid, hipStream_t s) {
 
 }  // namespace
 
-hipError_t launch_attn_bf16(const AttnParams &p, int head_dim, int mode, int grid, hipStream_t s) {
-    return head_dim == 128 ? launch_d<128>(p, mode, grid, s) : launch_d<64>(p, mode, grid, s);
+hipError_t launch_attn_bf16(const AttnParams &p, int head_dim, int mode, bool f16, int grid, hipStream_t s) {
+    if (f16) return head_dim == 128 ? launch_d<128, F16>(p, mode, grid, s) : launch_d<64, F16>(p, mode, grid, s);
+    return head_dim == 128 ? launch_d<128, Bf16>(p, mode, grid, s) : launch_d<64, Bf16>(p, mode, grid, s);
 }
 
 

@@ -24,6 +24,8 @@ namespace dev {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
@@ -51,6 +53,28 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
 }
 
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
+
+// The two 16-bit element formats of the MFMA path (the descriptor's dtype):
+// the matrix product on 8 elements per lane, and the round-to-nearest-even
+// packing used for P and for the output rows.
+struct Bf16 {
+    __device__ static __forceinline__ f32x16 mfma(u32x4 a, u32x4 b, f32x16 c) {
+        return __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a), as_bf16x8(b), c, 0, 0, 0);
+    }
+    __device__ static __forceinline__ uint32_t pack2(float lo, float hi) { return pack_bf16x2(lo, hi); }
+};
+struct F16 {
+    __device__ static __forceinline__ f32x16 mfma(u32x4 a, u32x4 b, f32x16 c) {
+        return __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, a), __builtin_bit_cast(f16x8, b), c,
+                                                      0, 0, 0);
+    }
+    __device__ static __forceinline__ uint32_t pack2(float lo, float hi) {
+        f16x2 v;
+        v[0] = (_Float16)lo;
+        v[1] = (_Float16)hi;
+        return __builtin_bit_cast(uint32_t, v);
+    }
+};
 
 // Lanes l and l^32 hold the two halves of one query row.  v_permlane32_swap
 // exchanges the upper half of its first operand with the lower half of its
@@ -194,7 +218,7 @@ __device__ __forceinline__ void wait_vmcnt() {
 //   vaddr(st, kk, h, mt)  LDS byte address this lane passes to the transposing
 //                         read for keys 32*st + 16*kk + 8*h + 4*(g16/2) .. +3
 //   lim                   keys with tile offset > lim are masked (only if mask)
-template <int D, int NSUB = 2, class KA, class VA>
+template <class E, int D, int NSUB = 2, class KA, class VA>
 __device__ __forceinline__ void tile_step(RowState<D> &rs, const u32x4 (&qf)[D / 16], KA kaddr, VA vaddr,
                                           bool mask, int lim, float c2, int grp) {
     f32x16 s[NSUB];
@@ -215,7 +239,7 @@ __device__ __forceinline__ void tile_step(RowState<D> &rs, const u32x4 (&qf)[D /
         }
 #pragma unroll
         for (int st = 0; st < NSUB; ++st)
-            s[st] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a[ks & 1][st]), as_bf16x8(qf[ks]), s[st], 0, 0, 0);
+            s[st] = E::mfma(a[ks & 1][st], qf[ks], s[st]);
     }
     // causal mask: tile key offset 32*st + 8*(i/4) + 4*grp + i%4 is visible iff <= lim
     if (mask) {
@@ -253,7 +277,7 @@ __device__ __forceinline__ void tile_step(RowState<D> &rs, const u32x4 (&qf)[D /
         for (int i = 0; i < 16; i += 2) {
             const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[st][i], c2, -rs.m));
             const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[st][i + 1], c2, -rs.m));
-            const uint32_t pk = pack_bf16x2(p0, p1);
+            const uint32_t pk = E::pack2(p0, p1);
             // row sum in fp32 adds (a v_dot2 would wait behind MFMAs on the matrix pipe)
             lsum += p0 + p1;
             pf[st][i >> 3][(i & 7) >> 1] = pk;
@@ -271,28 +295,27 @@ __device__ __forceinline__ void tile_step(RowState<D> &rs, const u32x4 (&qf)[D /
                 const u32x2 lo2 = __builtin_bit_cast(u32x2, lo);
                 const u32x2 hi2 = __builtin_bit_cast(u32x2, hi);
                 const u32x4 a = {lo2[0], lo2[1], hi2[0], hi2[1]};
-                rs.o[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a), as_bf16x8(pf[st][kk]), rs.o[mt],
-                                                                  0, 0, 0);
+                rs.o[mt] = E::mfma(a, pf[st][kk], rs.o[mt]);
             }
 }
 
 // Final output (normalised, bf16) or split partial (unnormalised O, m, l).
-template <int D, int MODE>
+template <class E, int D, int MODE>
 __device__ __forceinline__ void epilogue(const AttnParams &p, const Work &w, const RowState<D> &rs, int r,
                                          bool valid, int tok, int head, int grp) {
     const float l_tot = pair_sum(rs.l);
     if (!valid) return;
     if (MODE != kModeContinue || p.nsplit == 1) {
         const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
-        __bf16 *orow = (__bf16 *)p.out + ((int64_t)(w.tok0 + tok) * p.n_q_heads + head) * D;
+        uint16_t *orow = (uint16_t *)p.out + ((int64_t)(w.tok0 + tok) * p.n_q_heads + head) * D;
 #pragma unroll
         for (int mt = 0; mt < D / 32; ++mt)
 #pragma unroll
             for (int q4 = 0; q4 < 4; ++q4) {
                 const int d = 32 * mt + 8 * q4 + 4 * grp;
                 u32x2 v;
-                v[0] = pack_bf16x2(rs.o[mt][4 * q4 + 0] * inv, rs.o[mt][4 * q4 + 1] * inv);
-                v[1] = pack_bf16x2(rs.o[mt][4 * q4 + 2] * inv, rs.o[mt][4 * q4 + 3] * inv);
+                v[0] = E::pack2(rs.o[mt][4 * q4 + 0] * inv, rs.o[mt][4 * q4 + 1] * inv);
+                v[1] = E::pack2(rs.o[mt][4 * q4 + 2] * inv, rs.o[mt][4 * q4 + 3] * inv);
                 *(u32x2 *)(orow + d) = v;
             }
     } else {

@@ -56,7 +56,7 @@ __device__ __forceinline__ int swz(int row) { return ((row >> 2) & 3) | ((row & 
 // 0..3 (the owner's own quarter comes from its registers, the others from
 // LDS), then stored -- bf16 output rows when there is no split, else the
 // split partial O quarter and, from the owner of quarter 0, (M, l).
-template <int NCT, int MT>
+template <class E, int NCT, int MT>
 __device__ __forceinline__ void finish_quarter(const AttnParams &p, const RowState<D> (&rs)[NCT],
                                                const float4 *obuf, const float *lbuf, const float *mbuf,
                                                const bool (&valid)[NCT], const int (&tok)[NCT],
@@ -105,12 +105,12 @@ __device__ __forceinline__ void finish_quarter(const AttnParams &p, const RowSta
         const int r = 32 * c + j;
         if (p.nsplit == 1) {
             const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
-            __bf16 *orow = (__bf16 *)p.out + ((int64_t)tok[c] * p.n_q_heads + head[c]) * D;
+            uint16_t *orow = (uint16_t *)p.out + ((int64_t)tok[c] * p.n_q_heads + head[c]) * D;
 #pragma unroll
             for (int q4 = 0; q4 < 4; ++q4) {
                 u32x2 v;
-                v[0] = pack_bf16x2(acc[4 * q4] * inv, acc[4 * q4 + 1] * inv);
-                v[1] = pack_bf16x2(acc[4 * q4 + 2] * inv, acc[4 * q4 + 3] * inv);
+                v[0] = E::pack2(acc[4 * q4] * inv, acc[4 * q4 + 1] * inv);
+                v[1] = E::pack2(acc[4 * q4 + 2] * inv, acc[4 * q4 + 3] * inv);
                 *(u32x2 *)(orow + 32 * MT + 8 * q4 + 4 * grp) = v;
             }
         } else {
@@ -157,8 +157,9 @@ __device__ __forceinline__ void codes_to_bf16(const u32x4 w, u32x4 &lo, u32x4 &h
 // are scaled by s_K inside the softmax exponent, the cached part of O by s_V
 // before the first new key (or at the end); the new rows stay bf16.  Cached
 // and new keys then never share a stage.
-template <int NCT, bool Q8>
+template <int NCT, bool Q8, class E>
 __global__ __launch_bounds__(THREADS) void attn_cont_kernel(const AttnParams p) {
+    static_assert(!Q8 || std::is_same<E, Bf16>::value, "the int8 artifact is a bf16 model's");
     __shared__ __attribute__((aligned(1024))) unsigned char smem[LDS_BYTES];
 
     const int tid = threadIdx.x;
@@ -375,8 +376,8 @@ __global__ __launch_bounds__(THREADS) void attn_cont_kernel(const AttnParams p) 
                 for (int c = 0; c < NCT; ++c) {
                     const u32x4 b0 = *(const u32x4 *)(qlds + 32 * c * ROWB + ka[2 * pr]);
                     const u32x4 b1 = *(const u32x4 *)(qlds + 32 * c * ROWB + ka[2 * pr + 1]);
-                    s[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a0), as_bf16x8(b0), s[c], 0, 0, 0);
-                    s[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a1), as_bf16x8(b1), s[c], 0, 0, 0);
+                    s[c] = E::mfma(a0, b0, s[c]);
+                    s[c] = E::mfma(a1, b1, s[c]);
                 }
             }
         } else {
@@ -387,7 +388,7 @@ __global__ __launch_bounds__(THREADS) void attn_cont_kernel(const AttnParams p) 
                 for (int c = 0; c < NCT; ++c) {
                     // Q row 32*c + j has the same swizzle as row j
                     const u32x4 b = *(const u32x4 *)(qlds + 32 * c * ROWB + ka[ks]);
-                    s[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a), as_bf16x8(b), s[c], 0, 0, 0);
+                    s[c] = E::mfma(a, b, s[c]);
                 }
             }
         }
@@ -426,7 +427,7 @@ __global__ __launch_bounds__(THREADS) void attn_cont_kernel(const AttnParams p) 
             for (int i = 0; i < 16; i += 2) {
                 const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[c][i], c2s, -rs[c].m));
                 const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[c][i + 1], c2s, -rs[c].m));
-                const uint32_t pk = pack_bf16x2(p0, p1);
+                const uint32_t pk = E::pack2(p0, p1);
                 lsum += p0 + p1;
                 pf[c][i >> 3][(i & 7) >> 1] = pk;
             }
@@ -443,10 +444,8 @@ __global__ __launch_bounds__(THREADS) void attn_cont_kernel(const AttnParams p) 
                 codes_to_bf16(w, a0, a1);
 #pragma unroll
                 for (int c = 0; c < NCT; ++c) {
-                    rs[c].o[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a0), as_bf16x8(pf[c][0]),
-                                                                         rs[c].o[mt], 0, 0, 0);
-                    rs[c].o[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a1), as_bf16x8(pf[c][1]),
-                                                                         rs[c].o[mt], 0, 0, 0);
+                    rs[c].o[mt] = E::mfma(a0, pf[c][0], rs[c].o[mt]);
+                    rs[c].o[mt] = E::mfma(a1, pf[c][1], rs[c].o[mt]);
                 }
             }
         } else {
@@ -463,8 +462,7 @@ __global__ __launch_bounds__(THREADS) void attn_cont_kernel(const AttnParams p) 
                     const u32x4 a = {lo2[0], lo2[1], hi2[0], hi2[1]};
 #pragma unroll
                     for (int c = 0; c < NCT; ++c)
-                        rs[c].o[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a), as_bf16x8(pf[c][kk]),
-                                                                             rs[c].o[mt], 0, 0, 0);
+                        rs[c].o[mt] = E::mfma(a, pf[c][kk], rs[c].o[mt]);
                 }
         }
     };
@@ -500,29 +498,28 @@ __global__ __launch_bounds__(THREADS) void attn_cont_kernel(const AttnParams p) 
     }
     __syncthreads();
     switch (wave) {
-        case 0: finish_quarter<NCT, 0>(p, rs, obuf, lbuf, mbuf, valid, tok, head, g, split, lane); break;
-        case 1: finish_quarter<NCT, 1>(p, rs, obuf, lbuf, mbuf, valid, tok, head, g, split, lane); break;
-        case 2: finish_quarter<NCT, 2>(p, rs, obuf, lbuf, mbuf, valid, tok, head, g, split, lane); break;
-        default: finish_quarter<NCT, 3>(p, rs, obuf, lbuf, mbuf, valid, tok, head, g, split, lane); break;
+        case 0: finish_quarter<E, NCT, 0>(p, rs, obuf, lbuf, mbuf, valid, tok, head, g, split, lane); break;
+        case 1: finish_quarter<E, NCT, 1>(p, rs, obuf, lbuf, mbuf, valid, tok, head, g, split, lane); break;
+        case 2: finish_quarter<E, NCT, 2>(p, rs, obuf, lbuf, mbuf, valid, tok, head, g, split, lane); break;
+        default: finish_quarter<E, NCT, 3>(p, rs, obuf, lbuf, mbuf, valid, tok, head, g, split, lane); break;
     }
 }
 
 }  // namespace
 
-hipError_t launch_attn_cont(const AttnParams &p, int ncol_tiles, bool q8, int grid, hipStream_t s) {
-    if (q8) {
-        switch (ncol_tiles) {
-            case 1: hipLaunchKernelGGL((attn_cont_kernel<1, true>), dim3(grid), dim3(THREADS), 0, s, p); break;
-            case 2: hipLaunchKernelGGL((attn_cont_kernel<2, true>), dim3(grid), dim3(THREADS), 0, s, p); break;
-            default: hipLaunchKernelGGL((attn_cont_kernel<3, true>), dim3(grid), dim3(THREADS), 0, s, p); break;
-        }
-    } else {
-        switch (ncol_tiles) {
-            case 1: hipLaunchKernelGGL((attn_cont_kernel<1, false>), dim3(grid), dim3(THREADS), 0, s, p); break;
-            case 2: hipLaunchKernelGGL((attn_cont_kernel<2, false>), dim3(grid), dim3(THREADS), 0, s, p); break;
-            default: hipLaunchKernelGGL((attn_cont_kernel<3, false>), dim3(grid), dim3(THREADS), 0, s, p); break;
-        }
+template <bool Q8, class E>
+void launch_nct(const AttnParams &p, int ncol_tiles, int grid, hipStream_t s) {
+    switch (ncol_tiles) {
+        case 1: hipLaunchKernelGGL((attn_cont_kernel<1, Q8, E>), dim3(grid), dim3(THREADS), 0, s, p); break;
+        case 2: hipLaunchKernelGGL((attn_cont_kernel<2, Q8, E>), dim3(grid), dim3(THREADS), 0, s, p); break;
+        default: hipLaunchKernelGGL((attn_cont_kernel<3, Q8, E>), dim3(grid), dim3(THREADS), 0, s, p); break;
     }
+}
+
+hipError_t launch_attn_cont(const AttnParams &p, int ncol_tiles, bool q8, bool f16, int grid, hipStream_t s) {
+    if (q8) launch_nct<true, Bf16>(p, ncol_tiles, grid, s);
+    else if (f16) launch_nct<false, F16>(p, ncol_tiles, grid, s);
+    else launch_nct<false, Bf16>(p, ncol_tiles, grid, s);
     return hipGetLastError();
 }
 

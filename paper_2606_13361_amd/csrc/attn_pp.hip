@@ -54,7 +54,7 @@ struct TileSrc {
     int on;           // 1: the loads run; 0: they run with no lane enabled
 };
 
-template <int MODE>
+template <int MODE, class E>
 __global__ __launch_bounds__(PP_THREADS) void attn_pp_kernel(const AttnParams p) {
     __shared__ __attribute__((aligned(1024))) unsigned char smem[NS * STAGE];
 
@@ -94,7 +94,7 @@ __global__ __launch_bounds__(PP_THREADS) void attn_pp_kernel(const AttnParams p)
 
     u32x4 qf[D / 16];
     {
-        const __bf16 *qrow = (const __bf16 *)p.q + ((int64_t)(tok0 + tok) * p.n_q_heads + head) * D;
+        const uint16_t *qrow = (const uint16_t *)p.q + ((int64_t)(tok0 + tok) * p.n_q_heads + head) * D;
 #pragma unroll
         for (int ks = 0; ks < D / 16; ++ks)
             qf[ks] = valid ? *(const u32x4 *)(qrow + 16 * ks + 8 * grp) : (u32x4){0, 0, 0, 0};
@@ -217,10 +217,10 @@ __global__ __launch_bounds__(PP_THREADS) void attn_pp_kernel(const AttnParams p)
     };
     auto pv = [&](const u32x4 &a, int idx) {
         const int st = idx >> 3, kk = (idx >> 2) & 1, mt = idx & 3;
-        rs.o[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a), as_bf16x8(pf[st][kk]), rs.o[mt], 0, 0, 0);
+        rs.o[mt] = E::mfma(a, pf[st][kk], rs.o[mt]);
     };
     auto sm = [&](const u32x4 &a, int st, int ks) {
-        s[st] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a), as_bf16x8(qf[ks]), s[st], 0, 0, 0);
+        s[st] = E::mfma(a, qf[ks], s[st]);
     };
     auto s_zero = [&]() {
 #pragma unroll
@@ -295,7 +295,7 @@ __global__ __launch_bounds__(PP_THREADS) void attn_pp_kernel(const AttnParams p)
                 for (int i = 0; i < 16; i += 2) {
                     const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[st][i], c2, -rs.m));
                     const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[st][i + 1], c2, -rs.m));
-                    const uint32_t pk = pack_bf16x2(p0, p1);
+                    const uint32_t pk = E::pack2(p0, p1);
                     // row sums with plain fp32 adds: a v_dot2 would queue behind the
                     // other wave's MFMAs on the matrix pipe and stall this wave
                     float &acc = lsum[(i >> 1) & 3];
@@ -453,8 +453,8 @@ __global__ __launch_bounds__(PP_THREADS) void attn_pp_kernel(const AttnParams p)
 #pragma unroll
             for (int q4 = 0; q4 < 4; ++q4) {
                 u32x2 v;
-                v[0] = pack_bf16x2(rs.o[mt][4 * q4] * inv, rs.o[mt][4 * q4 + 1] * inv);
-                v[1] = pack_bf16x2(rs.o[mt][4 * q4 + 2] * inv, rs.o[mt][4 * q4 + 3] * inv);
+                v[0] = E::pack2(rs.o[mt][4 * q4] * inv, rs.o[mt][4 * q4 + 1] * inv);
+                v[1] = E::pack2(rs.o[mt][4 * q4 + 2] * inv, rs.o[mt][4 * q4 + 3] * inv);
                 *(u32x2 *)(ob + j * OPITCH + 2 * (32 * mt + 8 * q4 + 4 * grp)) = v;
             }
         asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // this wave's rows are in LDS
@@ -464,7 +464,7 @@ __global__ __launch_bounds__(PP_THREADS) void attn_pp_kernel(const AttnParams p)
             const int rw = wrow0 + rr;
             if (rw < R) {
                 const u32x4 v = *(const u32x4 *)(ob + rr * OPITCH + 16 * (lane & 15));
-                __bf16 *orow = (__bf16 *)p.out + ((int64_t)(tok0 + rw / G) * p.n_q_heads + g * G + rw % G) * D;
+                uint16_t *orow = (uint16_t *)p.out + ((int64_t)(tok0 + rw / G) * p.n_q_heads + g * G + rw % G) * D;
                 *(u32x4 *)(orow + 8 * (lane & 15)) = v;
             }
         }
@@ -473,11 +473,14 @@ __global__ __launch_bounds__(PP_THREADS) void attn_pp_kernel(const AttnParams p)
 
 }  // namespace
 
-hipError_t launch_attn_pp(const AttnParams &p, int mode, int grid, hipStream_t s) {
-    if (mode == kModePrefill)
-        hipLaunchKernelGGL(attn_pp_kernel<kModePrefill>, dim3(grid), dim3(PP_THREADS), 0, s, p);
-    else
-        hipLaunchKernelGGL(attn_pp_kernel<kModeReaders>, dim3(grid), dim3(PP_THREADS), 0, s, p);
+hipError_t launch_attn_pp(const AttnParams &p, int mode, bool f16, int grid, hipStream_t s) {
+    if (mode == kModePrefill) {
+        if (f16) hipLaunchKernelGGL((attn_pp_kernel<kModePrefill, F16>), dim3(grid), dim3(PP_THREADS), 0, s, p);
+        else hipLaunchKernelGGL((attn_pp_kernel<kModePrefill, Bf16>), dim3(grid), dim3(PP_THREADS), 0, s, p);
+    } else {
+        if (f16) hipLaunchKernelGGL((attn_pp_kernel<kModeReaders, F16>), dim3(grid), dim3(PP_THREADS), 0, s, p);
+        else hipLaunchKernelGGL((attn_pp_kernel<kModeReaders, Bf16>), dim3(grid), dim3(PP_THREADS), 0, s, p);
+    }
     return hipGetLastError();
 }
 

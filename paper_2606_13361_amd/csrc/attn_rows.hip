@@ -60,6 +60,7 @@ __device__ __forceinline__ void wait_stages(int k) {
 }
 static_assert(NS - 2 <= 6, "wait_stages covers at most six stages in flight");
 
+template <class E>
 __global__ __launch_bounds__(RTHREADS) void attn_rows_kernel(const AttnParams p) {
     __shared__ __attribute__((aligned(1024))) unsigned char smem[LDS_BYTES];
 
@@ -209,8 +210,8 @@ __global__ __launch_bounds__(RTHREADS) void attn_rows_kernel(const AttnParams p)
         for (int i = 0; i < 16; ++i) sa[i] = sb[i] = 0.f;
 #pragma unroll
         for (int ks = 0; ks < D / 16; ks += 2) {
-            sa = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kf[ks]), as_bf16x8(qf[ks]), sa, 0, 0, 0);
-            sb = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kf[ks + 1]), as_bf16x8(qf[ks + 1]), sb, 0, 0, 0);
+            sa = E::mfma(kf[ks], qf[ks], sa);
+            sb = E::mfma(kf[ks + 1], qf[ks + 1], sb);
         }
         float sv[16];
 #pragma unroll
@@ -228,7 +229,7 @@ __global__ __launch_bounds__(RTHREADS) void attn_rows_kernel(const AttnParams p)
             for (int i = 0; i < 16; i += 2) {
                 const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(sv[i], c2, -rs.m));
                 const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(sv[i + 1], c2, -rs.m));
-                pf[i >> 3][(i & 7) >> 1] = pack_bf16x2(p0, p1);
+                pf[i >> 3][(i & 7) >> 1] = E::pack2(p0, p1);
                 ls[(i >> 1) & 1] += p0 + p1;
             }
             return ls[0] + ls[1];
@@ -256,7 +257,7 @@ __global__ __launch_bounds__(RTHREADS) void attn_rows_kernel(const AttnParams p)
 #pragma unroll
         for (int idx = 0; idx < 8; ++idx) {
             const int kk = idx >> 2, mt = idx & 3;
-            rs.o[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(vf[idx]), as_bf16x8(pf[kk]), rs.o[mt], 0, 0, 0);
+            rs.o[mt] = E::mfma(vf[idx], pf[kk], rs.o[mt]);
         }
     };
 
@@ -328,14 +329,14 @@ __global__ __launch_bounds__(RTHREADS) void attn_rows_kernel(const AttnParams p)
     if (!valid) return;
     if (p.nsplit == 1) {
         const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
-        __bf16 *orow = (__bf16 *)p.out + ((int64_t)tok * p.n_q_heads + head) * D;
+        uint16_t *orow = (uint16_t *)p.out + ((int64_t)tok * p.n_q_heads + head) * D;
 #pragma unroll
         for (int mt = 0; mt < D / 32; ++mt)
 #pragma unroll
             for (int q4 = 0; q4 < 4; ++q4) {
                 u32x2 v;
-                v[0] = pack_bf16x2(rs.o[mt][4 * q4] * inv, rs.o[mt][4 * q4 + 1] * inv);
-                v[1] = pack_bf16x2(rs.o[mt][4 * q4 + 2] * inv, rs.o[mt][4 * q4 + 3] * inv);
+                v[0] = E::pack2(rs.o[mt][4 * q4] * inv, rs.o[mt][4 * q4 + 1] * inv);
+                v[1] = E::pack2(rs.o[mt][4 * q4 + 2] * inv, rs.o[mt][4 * q4 + 3] * inv);
                 *(u32x2 *)(orow + 32 * mt + 8 * q4 + 4 * grp) = v;
             }
     } else {
@@ -356,8 +357,9 @@ __global__ __launch_bounds__(RTHREADS) void attn_rows_kernel(const AttnParams p)
 
 }  // namespace
 
-hipError_t launch_attn_rows(const AttnParams &p, int grid, hipStream_t s) {
-    hipLaunchKernelGGL(attn_rows_kernel, dim3(grid), dim3(RTHREADS), 0, s, p);
+hipError_t launch_attn_rows(const AttnParams &p, bool f16, int grid, hipStream_t s) {
+    if (f16) hipLaunchKernelGGL(attn_rows_kernel<F16>, dim3(grid), dim3(RTHREADS), 0, s, p);
+    else hipLaunchKernelGGL(attn_rows_kernel<Bf16>, dim3(grid), dim3(RTHREADS), 0, s, p);
     return hipGetLastError();
 }
 

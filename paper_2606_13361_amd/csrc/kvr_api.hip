@@ -22,20 +22,24 @@ constexpr int64_t kMinSplitKeys = 256;
 // longest key range per workgroup for which the row-split continuation is used
 constexpr int64_t kRowsSplitMaxKeys = 640;
 
+// bf16 and fp16 share the 16-bit MFMA path; f16() picks the element format
+bool is16(const kvr_desc *d) { return d->dtype == KVR_BF16 || d->dtype == KVR_F16; }
+bool f16(const kvr_desc *d) { return d->dtype == KVR_F16; }
+
 // Continuations of at most kContMaxRows query rows per kv head (decode steps,
 // short suffixes) at bf16 / head_dim 128 use the kernel whose waves split the keys.
 bool use_cont(const kvr_desc *d, int64_t S) {
-    return d->dtype == KVR_BF16 && d->head_dim == 128 && (int64_t)(d->n_q_heads / d->n_kv_heads) * S <= kContMaxRows;
+    return is16(d) && d->head_dim == 128 && (int64_t)(d->n_q_heads / d->n_kv_heads) * S <= kContMaxRows;
 }
 
 // Prefill and many readers at bf16 / head_dim 128 use the two-group kernel.
-bool use_pp(const kvr_desc *d) { return d->dtype == KVR_BF16 && d->head_dim == 128; }
+bool use_pp(const kvr_desc *d) { return is16(d) && d->head_dim == 128; }
 
 bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
 
 int check_desc(const kvr_desc *d) {
     if (!d) return KVR_ERR_NULL;
-    if (d->dtype != KVR_BF16 && d->dtype != KVR_F32) return KVR_ERR_DTYPE;
+    if (d->dtype != KVR_BF16 && d->dtype != KVR_F32 && d->dtype != KVR_F16) return KVR_ERR_DTYPE;
     if (d->n_q_heads <= 0 || d->n_kv_heads <= 0 || d->n_q_heads % d->n_kv_heads != 0) return KVR_ERR_SHAPE;
     if (d->n_q_heads > 4096) return KVR_ERR_SHAPE;
     if (d->head_dim != 64 && d->head_dim != 128) return KVR_ERR_SHAPE;
@@ -47,9 +51,9 @@ int check_desc(const kvr_desc *d) {
 
 float eff_scale(const kvr_desc *d) { return d->scale > 0.f ? d->scale : 1.f / sqrtf((float)d->head_dim); }
 
-int elt_bytes(const kvr_desc *d) { return d->dtype == KVR_BF16 ? 2 : 4; }
+int elt_bytes(const kvr_desc *d) { return is16(d) ? 2 : 4; }
 
-int rows_per_tile(const kvr_desc *d) { return d->dtype == KVR_BF16 ? kRowsBf16 : kRowsF32; }
+int rows_per_tile(const kvr_desc *d) { return is16(d) ? kRowsBf16 : kRowsF32; }
 
 struct Split {
     int32_t nsplit;
@@ -61,7 +65,7 @@ struct Split {
 // every split a whole number of key tiles.  A pure function of the shape.
 Split plan_split(const kvr_desc *d, int64_t L_prefix, int64_t S) {
     Split s{1, 0, 0};
-    if (d->dtype != KVR_BF16 || L_prefix <= 0 || S <= 0) return s;
+    if (!is16(d) || L_prefix <= 0 || S <= 0) return s;
     const int64_t G = d->n_q_heads / d->n_kv_heads;
     const int64_t rows = G * S;
     const int64_t tiles = (rows + kRowsBf16 - 1) / kRowsBf16;
@@ -158,15 +162,15 @@ int launch_single(const kvr_desc *d, int mode, const void *Q, const void *K, con
         const int nct = (int)((rows + 31) / 32);
         const int64_t keys_per_wg = p.nsplit > 1 ? p.chunk : n_prefix + n_tok;
         if (qscale || nct == 1 || keys_per_wg > kRowsSplitMaxKeys)
-            e = launch_attn_cont(p, nct, qscale != nullptr, (int)grid, stream);
+            e = launch_attn_cont(p, nct, qscale != nullptr, f16(d), (int)grid, stream);
         else
-            e = launch_attn_rows(p, (int)grid, stream);
+            e = launch_attn_rows(p, f16(d), (int)grid, stream);
     } else if (mode == kModePrefill && use_pp(d)) {
         const int64_t pp_tiles = (rows + kRowsPP - 1) / kRowsPP;
         p.tiles_total = (int32_t)pp_tiles;
-        e = launch_attn_pp(p, kModePrefill, (int)(pp_tiles * p.n_kv_heads), stream);
-    } else if (d->dtype == KVR_BF16) {
-        e = launch_attn_bf16(p, d->head_dim, mode, (int)grid, stream);
+        e = launch_attn_pp(p, kModePrefill, f16(d), (int)(pp_tiles * p.n_kv_heads), stream);
+    } else if (is16(d)) {
+        e = launch_attn_bf16(p, d->head_dim, mode, f16(d), (int)grid, stream);
     } else {
         if (mode == kModePrefill) {   // the fp32 kernel does not write the cache itself
             const int st = append_impl(d, K, V, n_tok, kc, vc, 0, stream);
@@ -179,7 +183,7 @@ int launch_single(const kvr_desc *d, int mode, const void *Q, const void *K, con
         MergeParams m;
         m.ws = p.ws; m.out = out; m.nsplit = p.nsplit; m.n_q_heads = p.n_q_heads;
         m.n_kv_heads = p.n_kv_heads; m.group = p.group; m.rows = (int32_t)rows;
-        e = launch_merge_bf16(m, d->head_dim, stream);
+        e = launch_merge_bf16(m, d->head_dim, f16(d), stream);
         if (e != hipSuccess) return KVR_ERR_DEVICE;
     }
     return KVR_OK;
@@ -352,10 +356,10 @@ int kvr_continue_batched(const kvr_desc *desc, const void *Qs, const void *Ks, c
         p.tiles_total = tiles;
         p.rows_total = 0;
         const int64_t grid = (int64_t)tiles * p.n_kv_heads;
-        hipError_t e = use_pp(desc) ? launch_attn_pp(p, kModeReaders, (int)grid, (hipStream_t)stream)
-                       : desc->dtype == KVR_BF16 ? launch_attn_bf16(p, desc->head_dim, kModeReaders, (int)grid,
-                                                                    (hipStream_t)stream)
-                                               : launch_attn_f32(p, desc->head_dim, (int)grid, (hipStream_t)stream);
+        hipError_t e = use_pp(desc) ? launch_attn_pp(p, kModeReaders, f16(desc), (int)grid, (hipStream_t)stream)
+                       : is16(desc) ? launch_attn_bf16(p, desc->head_dim, kModeReaders, f16(desc), (int)grid,
+                                                       (hipStream_t)stream)
+                                    : launch_attn_f32(p, desc->head_dim, (int)grid, (hipStream_t)stream);
         if (e != hipSuccess) return KVR_ERR_DEVICE;
     }
     return KVR_OK;

@@ -70,18 +70,19 @@ struct MergeParams {
 enum { kModePrefill = 0, kModeContinue = 1, kModeReaders = 2 };
 
 // bf16 path (MFMA), D in {64, 128}
-hipError_t launch_attn_bf16(const AttnParams &p, int head_dim, int mode, int grid, hipStream_t s);
-hipError_t launch_merge_bf16(const MergeParams &p, int head_dim, hipStream_t s);
+// (the 16-bit MFMA path: f16 selects fp16 elements, else bf16)
+hipError_t launch_attn_bf16(const AttnParams &p, int head_dim, int mode, bool f16, int grid, hipStream_t s);
+hipError_t launch_merge_bf16(const MergeParams &p, int head_dim, bool f16, hipStream_t s);
 // bf16 prefill and many readers at D = 128: two groups of 4 waves alternate
 // matrix and softmax steps
 constexpr int kRowsPP = 256;   // query rows per workgroup (8 waves x 32)
-hipError_t launch_attn_pp(const AttnParams &p, int mode, int grid, hipStream_t s);
+hipError_t launch_attn_pp(const AttnParams &p, int mode, bool f16, int grid, hipStream_t s);
 // bf16 continuation for G*S <= 96 rows (D = 128).  33..96 rows: the waves of
 // a workgroup split the rows and share one ring of key stages; up to 32 rows
 // (decode steps) and the int8 artifact: the waves split the keys
 constexpr int kContMaxRows = 96;
-hipError_t launch_attn_rows(const AttnParams &p, int grid, hipStream_t s);
-hipError_t launch_attn_cont(const AttnParams &p, int ncol_tiles, bool q8, int grid, hipStream_t s);
+hipError_t launch_attn_rows(const AttnParams &p, bool f16, int grid, hipStream_t s);
+hipError_t launch_attn_cont(const AttnParams &p, int ncol_tiles, bool q8, bool f16, int grid, hipStream_t s);
 // int8 artifact
 hipError_t launch_quantize(const QuantParams &p, hipStream_t s);
 // fp32 path (VALU), D in {64, 128}

@@ -1,4 +1,5 @@
 // merge.hip -- combine the per-split partial results of a split continuation
+// (16-bit outputs: bf16 or fp16 as the descriptor says)
 // (fixed split order, so the result is reproducible bit for bit):
 //   M = max_s m_s,  w_s = 2^(m_s - M),  out = sum_s w_s O_s / sum_s w_s l_s
 // which is the log-sum-exp merge of partial softmax sums.
@@ -22,7 +23,7 @@ using namespace dev;
 constexpr int MERGE_THREADS = 256;
 constexpr int MERGE_BATCH = 16;   // split loads in flight per lane
 
-template <int D>
+template <int D, class E>
 __global__ __launch_bounds__(MERGE_THREADS) void merge_bf16_kernel(const MergeParams p) {
     constexpr int CPR = D / 4;                 // lanes per row
     constexpr int RPW = MERGE_THREADS / CPR;   // rows per workgroup
@@ -82,22 +83,25 @@ __global__ __launch_bounds__(MERGE_THREADS) void merge_bf16_kernel(const MergePa
     const float il = l > 0.f ? 1.f / l : 0.f;
     const int tok = r / p.group;
     const int head = g * p.group + r % p.group;
-    __bf16 *out = (__bf16 *)p.out + ((int64_t)tok * p.n_q_heads + head) * D + 4 * part;
+    uint16_t *out = (uint16_t *)p.out + ((int64_t)tok * p.n_q_heads + head) * D + 4 * part;
     u32x2 v;
-    v[0] = pack_bf16x2(acc.x * il, acc.y * il);
-    v[1] = pack_bf16x2(acc.z * il, acc.w * il);
+    v[0] = E::pack2(acc.x * il, acc.y * il);
+    v[1] = E::pack2(acc.z * il, acc.w * il);
     *(u32x2 *)out = v;
 }
 
 }  // namespace
 
-hipError_t launch_merge_bf16(const MergeParams &p, int head_dim, hipStream_t s) {
+hipError_t launch_merge_bf16(const MergeParams &p, int head_dim, bool f16, hipStream_t s) {
     const int rpw = MERGE_THREADS / (head_dim / 4);
     const int grid = (p.rows + rpw - 1) / rpw * p.n_kv_heads;
-    if (head_dim == 128)
-        hipLaunchKernelGGL(merge_bf16_kernel<128>, dim3(grid), dim3(MERGE_THREADS), 0, s, p);
-    else
-        hipLaunchKernelGGL(merge_bf16_kernel<64>, dim3(grid), dim3(MERGE_THREADS), 0, s, p);
+    if (head_dim == 128) {
+        if (f16) hipLaunchKernelGGL((merge_bf16_kernel<128, F16>), dim3(grid), dim3(MERGE_THREADS), 0, s, p);
+        else hipLaunchKernelGGL((merge_bf16_kernel<128, Bf16>), dim3(grid), dim3(MERGE_THREADS), 0, s, p);
+    } else {
+        if (f16) hipLaunchKernelGGL((merge_bf16_kernel<64, F16>), dim3(grid), dim3(MERGE_THREADS), 0, s, p);
+        else hipLaunchKernelGGL((merge_bf16_kernel<64, Bf16>), dim3(grid), dim3(MERGE_THREADS), 0, s, p);
+    }
     return hipGetLastError();
 }
 

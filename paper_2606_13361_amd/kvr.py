@@ -19,14 +19,14 @@ KVR_OK, KVR_ERR_NULL, KVR_ERR_SHAPE, KVR_ERR_DTYPE = 0, 1, 2, 3
 KVR_ERR_CAPACITY, KVR_ERR_WORKSPACE, KVR_ERR_ALIGN, KVR_ERR_DEVICE = 4, 5, 6, 7
 KVR_ERR_MISMATCH = 8
 KVR_ARTIFACT_HEADER_BYTES = 256
-KVR_BF16, KVR_F32 = 0, 1
+KVR_BF16, KVR_F32, KVR_F16 = 0, 1, 2
 
 EXPORTS = ("kvr_prefill", "kvr_continue", "kvr_continue_batched", "kvr_cache_append",
            "kvr_workspace_bytes", "kvr_strerror", "kvr_abi_version",
            "kvr_q8_bytes", "kvr_quantize_cache", "kvr_continue_q8",
            "kvr_artifact_bytes", "kvr_artifact_save", "kvr_artifact_load")
 
-_TORCH_DTYPE = {KVR_BF16: torch.bfloat16, KVR_F32: torch.float32}
+_TORCH_DTYPE = {KVR_BF16: torch.bfloat16, KVR_F32: torch.float32, KVR_F16: torch.float16}
 
 
 class kvr_desc(ctypes.Structure):
@@ -93,9 +93,9 @@ def kvr_abi_version():
 
 
 def make_desc(n_q_heads, n_kv_heads, head_dim, dtype, capacity, scale=0.0):
-    """dtype: torch.bfloat16 / torch.float32 or KVR_BF16 / KVR_F32."""
+    """dtype: torch.bfloat16 / torch.float16 / torch.float32 or KVR_BF16 / KVR_F16 / KVR_F32."""
     if isinstance(dtype, torch.dtype):
-        dtype = {torch.bfloat16: KVR_BF16, torch.float32: KVR_F32}.get(dtype, -1)
+        dtype = {torch.bfloat16: KVR_BF16, torch.float16: KVR_F16, torch.float32: KVR_F32}.get(dtype, -1)
     return kvr_desc(int(n_q_heads), int(n_kv_heads), int(head_dim), int(dtype), float(scale), 0,
                     int(capacity))
 

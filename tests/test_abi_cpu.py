@@ -100,6 +100,7 @@ def batched(lib, d, cu, Lp=64, Q=A, K=A, V=A, kc=A, vc=A, out=A):
     (dict(head_dim=96), kvr.KVR_ERR_SHAPE),
     (dict(head_dim=256), kvr.KVR_ERR_SHAPE),
     (dict(dtype=7), kvr.KVR_ERR_DTYPE),
+    (dict(dtype=3), kvr.KVR_ERR_DTYPE),
     (dict(capacity=-1), kvr.KVR_ERR_SHAPE),
     (dict(scale=float("nan")), kvr.KVR_ERR_SHAPE),
 ])
@@ -110,6 +111,20 @@ def test_descriptor_errors(lib, bad, code):
     assert append(lib, d) == code
     assert batched(lib, d, [0, 4]) == code
     assert lib.kvr_workspace_bytes(ctypes.byref(d), 64, 8, 1) == ctypes.c_size_t(-1).value
+
+
+def test_fp16_descriptor(lib):
+    """fp16 (the paper's precision) is a valid dtype everywhere bf16 is, with the
+    same workspace; the int8 artifact is a bf16 model's only."""
+    d16, db = desc(dtype=kvr.KVR_F16), desc()
+    assert prefill(lib, d16, L=0, Q=None, K=None, V=None, out=None, kc=None, vc=None) == kvr.KVR_OK
+    assert cont(lib, d16, Lp=0, S=0) == kvr.KVR_OK
+    assert prefill(lib, d16, L=-1) == kvr.KVR_ERR_SHAPE
+    for Lp, S in ((3774, 24), (32768, 1), (100, 200)):
+        assert lib.kvr_workspace_bytes(ctypes.byref(d16), Lp, S, 1) == lib.kvr_workspace_bytes(ctypes.byref(db), Lp, S, 1)
+    assert quant(lib, d16) == kvr.KVR_ERR_DTYPE
+    assert cont_q8(lib, d16) == kvr.KVR_ERR_DTYPE
+    assert lib.kvr_artifact_bytes(ctypes.byref(d16), 36, 3774) == lib.kvr_artifact_bytes(ctypes.byref(db), 36, 3774)
 
 
 def test_null_descriptor(lib):
