@@ -97,3 +97,21 @@ def test_claim1_with_positions(Lp, S, Hq, Hkv):
     plain, _ = ref.continue_(Q[Lp:], K[Lp:], V[Lp:], np.transpose(K[:Lp], (1, 0, 2)).copy(), vc, Lp)
     want, _ = ref.prefill(Q, K, V, rows=list(range(Lp, n)))
     np.testing.assert_allclose(plain, want, rtol=0, atol=1e-12)
+
+
+@pytest.mark.parametrize("fmt", ["bf16", "fp16", "fp32"])
+def test_round_to_matches_torch(fmt):
+    """Rounding to the element format against torch's own conversion of fp32
+    values (a single correct rounding), including ties, subnormals of fp16 and
+    values just around rounding boundaries."""
+    import torch
+    tdt = {"bf16": torch.bfloat16, "fp16": torch.float16, "fp32": torch.float32}[fmt]
+    g = np.random.default_rng(11)
+    x = np.concatenate([g.standard_normal(20000), g.standard_normal(2000) * 1e-6,
+                        np.ldexp(g.integers(1, 4096, 2000).astype(np.float64), -30),
+                        [0.0, -0.0, 1.0, 1.0 + 2.0 ** -8, 1.0 + 3 * 2.0 ** -8, 1.0 + 2.0 ** -11,
+                         65504.0, 2.0 ** -24, 3 * 2.0 ** -25]]).astype(np.float32)
+    want = torch.from_numpy(x).to(tdt).to(torch.float64).numpy()
+    np.testing.assert_array_equal(rope.round_to(x.astype(np.float64), fmt), want)
+    assert rope.round_to(np.array([1.0 + 2.0 ** -8]), "bf16")[0] == 1.0        # tie to even
+    assert rope.round_to(np.array([1.0 + 3 * 2.0 ** -8]), "bf16")[0] == 1.0 + 2.0 ** -6
