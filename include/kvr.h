@@ -51,7 +51,7 @@
 extern "C" {
 #endif
 
-#define KVR_ABI_VERSION 2
+#define KVR_ABI_VERSION 3
 
 typedef enum {
     KVR_OK = 0,
@@ -62,8 +62,10 @@ typedef enum {
     KVR_ERR_WORKSPACE = 5, /* workspace smaller than kvr_workspace_bytes()         */
     KVR_ERR_ALIGN = 6,     /* a device pointer is not 16-byte aligned              */
     KVR_ERR_DEVICE = 7,    /* a HIP call or kernel launch failed                   */
-    KVR_ERR_MISMATCH = 8   /* an artifact's metadata does not match (model, dtype,
+    KVR_ERR_MISMATCH = 8,  /* an artifact's metadata does not match (model, dtype,
                               heads, head_dim, layers) or its header is not valid  */
+    KVR_ERR_POSITION = 9   /* a RoPE table without an entry for a position the call
+                              rotates, or invalid table arguments                  */
 } kvr_status;
 
 typedef enum { KVR_BF16 = 0, KVR_F32 = 1, KVR_F16 = 2 } kvr_dtype;
@@ -229,6 +231,93 @@ int kvr_artifact_save(const kvr_desc *desc, const char *model_id, int32_t n_laye
 int kvr_artifact_load(const kvr_desc *desc, const char *model_id, int32_t n_layers, const void *host,
                       size_t host_bytes, void *const *kcaches, void *const *vcaches, int64_t *L_out,
                       void *stream);
+
+/*
+ * Rotary position embedding with the position offset (paper, Section
+ * "Consuming an artifact": the continuation's tokens take positions L, L+1,
+ * ... after an artifact of length L, so that the positional encoding, e.g.
+ * RoPE, agrees with a pass from scratch).  The rotary embedding of Su et al.
+ * in the half-split pairing of the Qwen family: pair i in [0, d/2) of a head
+ * row is (x[i], x[i + d/2]); at position p it turns by the angle p * theta_i,
+ * theta_i = base^(-2 i / d):
+ *     y[i]       = x[i] cos - x[i + d/2] sin
+ *     y[i + d/2] = x[i + d/2] cos + x[i] sin
+ * Queries and keys are rotated, values are not, and the cache holds rotated
+ * keys (as the model's cache does).  The rotation runs in fp32 from the
+ * table's fp32 cos/sin and rounds once to the element format (16-bit: to
+ * nearest even); every entry point rotates a given row at a given position to
+ * the same bits.
+ *
+ * The table: float [n_pos][head_dim / 2][2] = (cos, sin) of p * theta_i in
+ * device memory (16-byte aligned), made by kvr_rope_table.  An entry point
+ * that rotates positions up to P needs n_pos > P (KVR_ERR_POSITION).
+ */
+typedef struct {
+    const float *cos_sin; /* device table [n_pos][head_dim / 2][2]            */
+    int64_t n_pos;        /* positions 0 .. n_pos - 1 it holds                  */
+} kvr_rope;
+
+/*
+ * Fill cos_sin [n_pos][head_dim / 2][2] for the given base on `stream`: the
+ * angle p * theta_i and its cosine and sine in fp64, each rounded once to
+ * fp32.  head_dim 64 or 128 (KVR_ERR_SHAPE), base finite and > 0, n_pos >= 0
+ * (KVR_ERR_POSITION); cos_sin 16-byte aligned.
+ */
+int kvr_rope_table(int32_t head_dim, double base, int64_t n_pos, float *cos_sin, void *stream);
+
+/*
+ * Rotate rows x [n_tok][n_heads][head_dim] (element type and head_dim from
+ * desc) at positions pos0 .. pos0 + n_tok - 1 into y (same layout; y == x
+ * rotates in place, other overlaps are not allowed).  n_heads > 0.  For
+ * callers that compose the other entry points themselves, e.g. rotated keys
+ * for kvr_cache_append or rotated Q/K for kvr_continue_q8.
+ */
+int kvr_rope_apply(const kvr_desc *desc, const kvr_rope *rope, const void *x, int64_t n_tok,
+                   int32_t n_heads, int64_t pos0, void *y, void *stream);
+
+/*
+ * kvr_prefill with RoPE: Q and K arrive unrotated, token t sits at position t.
+ * A pre-pass writes the rotated K rows and the V rows into kcache/vcache rows
+ * [0, L); the attention kernel reads the keys back from the cache and rotates
+ * each query row in registers.  Needs rope->n_pos >= L.
+ */
+int kvr_prefill_rope(const kvr_desc *desc, const kvr_rope *rope, const void *Q, const void *K,
+                     const void *V, int64_t L, void *out, void *kcache, void *vcache, void *stream);
+
+/*
+ * kvr_continue with RoPE (Alg. 2): Qs and Ks arrive unrotated and are rotated
+ * at positions L_prefix .. L_prefix + S - 1; kcache rows [0, L_prefix) hold
+ * rotated keys (from kvr_prefill_rope, an earlier call with append, or
+ * kvr_rope_apply + kvr_cache_append).  append != 0 also writes the rotated Ks
+ * and the Vs into cache rows [L_prefix, L_prefix + S) (a decode step in one
+ * call; needs L_prefix + S <= capacity); append == 0 leaves the cache
+ * untouched.  The rotated Qs/Ks rows go through ws:
+ * ws_bytes >= kvr_workspace_bytes_rope(desc, L_prefix, S, 1).
+ * Needs rope->n_pos >= L_prefix + S.
+ */
+int kvr_continue_rope(const kvr_desc *desc, const kvr_rope *rope, const void *Qs, const void *Ks,
+                      const void *Vs, void *kcache, void *vcache, int64_t L_prefix, int64_t S,
+                      int32_t append, void *out, void *ws, size_t ws_bytes, void *stream);
+
+/*
+ * kvr_continue_batched with RoPE: reader r's rows [cu[r], cu[r+1]) sit at
+ * positions L_prefix .. L_prefix + (cu[r+1] - cu[r]) - 1.  Their rotated keys
+ * go through ws (kvr_workspace_bytes_rope(desc, L_prefix, cu[n], n) bytes);
+ * query rows are rotated in registers.  The shared cache is only read.
+ * Needs rope->n_pos >= L_prefix + the longest reader.
+ */
+int kvr_continue_batched_rope(const kvr_desc *desc, const kvr_rope *rope, const void *Qs,
+                              const void *Ks, const void *Vs, const int32_t *cu_seqlens_host,
+                              int32_t n, const void *kcache, const void *vcache, int64_t L_prefix,
+                              void *out, void *ws, size_t ws_bytes, void *stream);
+
+/*
+ * Workspace bytes of kvr_continue_rope (n <= 1, total_S = S) and
+ * kvr_continue_batched_rope (n >= 2, total_S = cu[n]): the plain
+ * continuation's workspace plus room for the rotated rows.  Non-decreasing in
+ * L_prefix for a fixed total_S; (size_t)-1 for an invalid descriptor.
+ */
+size_t kvr_workspace_bytes_rope(const kvr_desc *desc, int64_t L_prefix, int64_t total_S, int32_t n);
 
 /*
  * Workspace bytes a continuation needs: n <= 1 for kvr_continue with

@@ -73,6 +73,8 @@ void attn_bf16_kernel(const AttnParams p) {
 #pragma unroll
         for (int ks = 0; ks < D / 16; ++ks)
             qf[ks] = valid ? *(const u32x4 *)(qrow + 16 * ks + 8 * grp) : (u32x4){0, 0, 0, 0};
+        // RoPE (prefill, readers): the row is rotated once, at its own position
+        if (p.rope && valid) rope_q_frag<E, D>(qf, p.rope + pos * D, grp);
     }
 
     // ---- staging map: thread -> 16-byte chunk sc of rows srow + RPP * i
@@ -80,9 +82,10 @@ void attn_bf16_kernel(const AttnParams p) {
     const int srow = tid / T::CH;
     const uint16_t *kc = (const uint16_t *)p.kc + (int64_t)g * p.cap * D + 8 * sc;
     const uint16_t *vc = (const uint16_t *)p.vc + (int64_t)g * p.cap * D + 8 * sc;
-    const int64_t nstride = (int64_t)p.n_kv_heads * D;
-    const uint16_t *kn = (const uint16_t *)p.kn + (int64_t)tok0 * nstride + (int64_t)g * D + 8 * sc;
-    const uint16_t *vn = (const uint16_t *)p.vn + (int64_t)tok0 * nstride + (int64_t)g * D + 8 * sc;
+    const int64_t nstride = p.new_tok_stride;
+    const int64_t nhead = p.new_head_stride * g;
+    const uint16_t *kn = (const uint16_t *)p.kn + (int64_t)tok0 * nstride + nhead + 8 * sc;
+    const uint16_t *vn = (const uint16_t *)p.vn + (int64_t)tok0 * nstride + nhead + 8 * sc;
     uint16_t *kco = (uint16_t *)p.kc_out + (int64_t)g * p.cap * D + 8 * sc;   // prefill: cache rows out
     uint16_t *vco = (uint16_t *)p.vc_out + (int64_t)g * p.cap * D + 8 * sc;
 
@@ -103,14 +106,14 @@ void attn_bf16_kernel(const AttnParams p) {
     }
     const int64_t cache_end = ke < npre ? ke : npre;   // keys [.., cache_end) come from the cache
     int64_t own_lo = 0, own_hi = -1;                   // prefill tokens whose cache row this WG stores
-    if constexpr (MODE == kModePrefill) {
+    if (MODE == kModePrefill && p.kc_out) {
         own_lo = (row0 + G - 1) / G;
         own_hi = (row0 + ROWS - 1) / G;
     }
     const unsigned char *kc0 = (const unsigned char *)p.kc + (int64_t)g * p.cap * D * 2;
     const unsigned char *vc0 = (const unsigned char *)p.vc + (int64_t)g * p.cap * D * 2;
-    const unsigned char *kn0 = (const unsigned char *)p.kn + ((int64_t)tok0 * nstride + (int64_t)g * D) * 2;
-    const unsigned char *vn0 = (const unsigned char *)p.vn + ((int64_t)tok0 * nstride + (int64_t)g * D) * 2;
+    const unsigned char *kn0 = (const unsigned char *)p.kn + ((int64_t)tok0 * nstride + nhead) * 2;
+    const unsigned char *vn0 = (const unsigned char *)p.vn + ((int64_t)tok0 * nstride + nhead) * 2;
     auto gload = [&](int64_t k0) {
         const bool own = MODE == kModePrefill && k0 <= own_hi && k0 + BN > own_lo;
         if (k0 + BN <= cache_end) {

@@ -62,6 +62,9 @@ struct Bf16 {
         return __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a), as_bf16x8(b), c, 0, 0, 0);
     }
     __device__ static __forceinline__ uint32_t pack2(float lo, float hi) { return pack_bf16x2(lo, hi); }
+    // the two elements of a packed word, widened exactly
+    __device__ static __forceinline__ float lo(uint32_t w) { return __uint_as_float(w << 16); }
+    __device__ static __forceinline__ float hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 };
 struct F16 {
     __device__ static __forceinline__ f32x16 mfma(u32x4 a, u32x4 b, f32x16 c) {
@@ -74,7 +77,45 @@ struct F16 {
         v[1] = (_Float16)hi;
         return __builtin_bit_cast(uint32_t, v);
     }
+    __device__ static __forceinline__ float lo(uint32_t w) { return (float)__builtin_bit_cast(f16x2, w)[0]; }
+    __device__ static __forceinline__ float hi(uint32_t w) { return (float)__builtin_bit_cast(f16x2, w)[1]; }
 };
+
+// Rotary position embedding of one pair (x1, x2) = (x[i], x[i + d/2]) by the
+// angle whose cosine and sine are c and s (rotary embedding of Su et al. in
+// the half-split pairing).  Written with explicit fused multiply-adds so that
+// every kernel that rotates a row (the key pre-pass, the in-register query
+// rotation) produces the same bits.
+__device__ __forceinline__ void rope_rot(float x1, float x2, float c, float s, float &y1, float &y2) {
+    y1 = __builtin_fmaf(x1, c, -(x2 * s));
+    y2 = __builtin_fmaf(x2, c, x1 * s);
+}
+
+// Rotate 8 + 8 packed elements: lo holds dims i0..i0+7, hi dims i0+d/2..; cs
+// points at the table entries (cos, sin) of dims i0..i0+7 at the row's position.
+template <class E>
+__device__ __forceinline__ void rope_rot8(u32x4 &lo, u32x4 &hi, const float *cs) {
+    const float4 *c4 = (const float4 *)cs;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+        const float4 t = c4[w];        // (cos, sin) of dims 2w and 2w + 1
+        float a1, a2, b1, b2;
+        rope_rot(E::lo(lo[w]), E::lo(hi[w]), t.x, t.y, a1, a2);
+        rope_rot(E::hi(lo[w]), E::hi(hi[w]), t.z, t.w, b1, b2);
+        lo[w] = E::pack2(a1, b1);
+        hi[w] = E::pack2(a2, b2);
+    }
+}
+
+// Query fragments in the matrix-core operand layout (qf[ks] holds dims
+// 16 ks + 8 grp .. +7 of the lane's row): the partner of dim i < d/2 is in
+// qf[ks + d/32] of the same lane, so the rotation needs no data exchange.
+// cs_row: the table row of the lane's position, (cos, sin) for dims 0..d/2-1.
+template <class E, int D>
+__device__ __forceinline__ void rope_q_frag(u32x4 (&qf)[D / 16], const float *cs_row, int grp) {
+#pragma unroll
+    for (int ks = 0; ks < D / 32; ++ks) rope_rot8<E>(qf[ks], qf[ks + D / 32], cs_row + 2 * (16 * ks + 8 * grp));
+}
 
 // Lanes l and l^32 hold the two halves of one query row.  v_permlane32_swap
 // exchanges the upper half of its first operand with the lower half of its

@@ -6,10 +6,12 @@
 // Workgroup: 64 query rows x 4 lanes per row; each lane owns a quarter of the
 // head dim of its row (q and the output accumulator live in registers).  Key
 // tiles of 32 rows are staged in LDS and read by every row of the workgroup.
-#include "kvr_internal.hpp"
+#include "attn_common.hpp"
 
 namespace kvr {
 namespace {
+
+using dev::rope_rot;
 
 constexpr int ROWS = kRowsF32;
 constexpr int LANES_PER_ROW = 4;
@@ -63,15 +65,30 @@ __global__ __launch_bounds__(THREADS) void attn_f32_kernel(const AttnParams p) {
             q[c] = valid ? qrow[c] : 0.f;
             o[c] = 0.f;
         }
+        // RoPE (prefill, readers): dim i < D/2 of the row pairs with dim
+        // i + D/2, which the lane two over (part + 2) holds
+        if (p.rope) {
+            const int half = part & 1;              // which DQ-slice of the pair index
+            const bool upper = part >= 2;
+            const float *cs = p.rope + (valid ? pos : 0) * D + 2 * half * DQ;
+#pragma unroll
+            for (int c = 0; c < DQ; ++c) {
+                const float other = __shfl_xor(q[c], 2);
+                float y1, y2;
+                if (upper) rope_rot(other, q[c], cs[2 * c], cs[2 * c + 1], y1, y2);
+                else rope_rot(q[c], other, cs[2 * c], cs[2 * c + 1], y1, y2);
+                if (valid) q[c] = upper ? y2 : y1;
+            }
+        }
     }
     float m_run = -INFINITY, l_run = 0.f;
     const float scale = p.scale;
 
     const float *kc = (const float *)p.kc + (int64_t)g * p.cap * D;
     const float *vc = (const float *)p.vc + (int64_t)g * p.cap * D;
-    const int64_t nstride = (int64_t)p.n_kv_heads * D;
-    const float *kn = (const float *)p.kn + (int64_t)tok0 * nstride + (int64_t)g * D;
-    const float *vn = (const float *)p.vn + (int64_t)tok0 * nstride + (int64_t)g * D;
+    const int64_t nstride = p.new_tok_stride;
+    const float *kn = (const float *)p.kn + (int64_t)tok0 * nstride + p.new_head_stride * g;
+    const float *vn = (const float *)p.vn + (int64_t)tok0 * nstride + p.new_head_stride * g;
 
     for (int64_t k0 = 0; k0 < ke; k0 += KT) {
         // stage KT key rows: float4 chunks, D/4 per row

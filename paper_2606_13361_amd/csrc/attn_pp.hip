@@ -98,15 +98,18 @@ __global__ __launch_bounds__(PP_THREADS) void attn_pp_kernel(const AttnParams p)
 #pragma unroll
         for (int ks = 0; ks < D / 16; ++ks)
             qf[ks] = valid ? *(const u32x4 *)(qrow + 16 * ks + 8 * grp) : (u32x4){0, 0, 0, 0};
+        // RoPE: the row is rotated once, at its own position
+        if (p.rope && valid) rope_q_frag<E, D>(qf, p.rope + (int64_t)pos * D, grp);
     }
 
     // ---- load map: wave w moves K rows 8w..8w+7 and V rows 8w..8w+7 of a tile,
     // 4 rows per instruction; lane -> row 8w + 4i + lane/16, LDS slot lane%16,
     // global chunk slot ^ swz(row)
-    const int64_t nstride_b = (int64_t)p.n_kv_heads * ROWB;
+    const int64_t nstride_b = p.new_tok_stride * 2;
+    const uint64_t nhead_b = (uint64_t)p.new_head_stride * 2 * g;
     // new rows of this segment (key npre + i is row tok0 + i), cached rows of head g
-    const uint64_t kn_a = (uint64_t)(uintptr_t)p.kn + (uint64_t)tok0 * nstride_b + (uint64_t)g * ROWB;
-    const uint64_t vn_a = (uint64_t)(uintptr_t)p.vn + (uint64_t)tok0 * nstride_b + (uint64_t)g * ROWB;
+    const uint64_t kn_a = (uint64_t)(uintptr_t)p.kn + (uint64_t)tok0 * nstride_b + nhead_b;
+    const uint64_t vn_a = (uint64_t)(uintptr_t)p.vn + (uint64_t)tok0 * nstride_b + nhead_b;
     const uint64_t kc_a = (uint64_t)(uintptr_t)p.kc + (uint64_t)g * p.cap * ROWB;
     const uint64_t vc_a = (uint64_t)(uintptr_t)p.vc + (uint64_t)g * p.cap * ROWB;
     int lrow[2];
@@ -421,7 +424,7 @@ __global__ __launch_bounds__(PP_THREADS) void attn_pp_kernel(const AttnParams p)
     // last NS tiles are still in it.
     __syncthreads();
 
-    if constexpr (MODE == kModePrefill) {
+    if constexpr (MODE == kModePrefill) if (p.kc_out) {
     // cache rows of the tokens whose first query row is in this workgroup, copied
     // from the ring: those tokens are the workgroup's last keys (at most 256/G + 1
     // of them, aligned so that they lie within the last four tiles)

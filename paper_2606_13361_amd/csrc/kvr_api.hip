@@ -100,6 +100,49 @@ void fill_common(AttnParams &p, const kvr_desc *d) {
     p.scale_log2 = p.scale * 1.4426950408889634f;
     p.cap = d->capacity;
     p.nsplit = 1;
+    p.new_tok_stride = (int64_t)d->n_kv_heads * d->head_dim;
+    p.new_head_stride = d->head_dim;
+}
+
+// RoPE table argument of a call that rotates positions [0, n_pos_needed)
+int check_rope(const kvr_rope *r, int64_t n_pos_needed) {
+    if (!r || !r->cos_sin) return KVR_ERR_NULL;
+    if (r->n_pos < 0 || r->n_pos < n_pos_needed) return KVR_ERR_POSITION;
+    if (!aligned16(r->cos_sin)) return KVR_ERR_ALIGN;
+    return KVR_OK;
+}
+
+size_t align256(size_t b) { return (b + 255) / 256 * 256; }
+
+// Workspace of the RoPE continuations: the plain split partials, then the
+// rotated query rows (single continuation only), then the rotated key rows.
+struct RopeWs {
+    size_t split, q_off, k_off, total;
+};
+RopeWs rope_ws(const kvr_desc *d, int64_t L_prefix, int64_t total_S, int32_t n) {
+    RopeWs w{0, 0, 0, 0};
+    const size_t row = (size_t)d->head_dim * elt_bytes(d);
+    if (n <= 1) {
+        w.split = align256(plan_split(d, L_prefix, total_S).ws_bytes);
+        w.q_off = w.split;
+        w.k_off = w.q_off + align256((size_t)total_S * d->n_q_heads * row);
+    }
+    w.total = w.k_off + align256((size_t)total_S * d->n_kv_heads * row);
+    return w;
+}
+
+// One pre-pass job over a single segment of n_tok rows at positions pos0..
+RopeParams rope_params(const kvr_desc *d, const kvr_rope *r, int64_t n_tok, int64_t pos0) {
+    RopeParams rp;
+    memset(&rp, 0, sizeof rp);
+    rp.cs = r->cos_sin;
+    rp.n_tok = n_tok;
+    rp.cap = d->capacity;
+    rp.pos0 = pos0;
+    rp.n_seg = 1;
+    rp.seg_tok0[0] = 0;
+    rp.seg_tok0[1] = (int32_t)(n_tok < 0x7fffffff ? n_tok : 0x7fffffff);
+    return rp;
 }
 
 // One segment: rows of tokens [0, n_tok).
@@ -116,14 +159,24 @@ int append_impl(const kvr_desc *d, const void *Ks, const void *Vs, int64_t S, vo
 // mode kModePrefill: kc/vc are the caches to fill (bf16: in the attention
 // kernel itself); kModeContinue: kc/vc are the cached prefix (read only).
 // qscale != NULL: continuation over the int8 artifact (kc/vc are its codes).
+// rope != NULL (prefill): rotate the query rows in registers, and read the
+// already rotated keys and the values back from kc/vc instead of K/V (the
+// RoPE pre-pass wrote them there); the kernel then writes no cache rows.
 int launch_single(const kvr_desc *d, int mode, const void *Q, const void *K, const void *V, void *kc,
                   void *vc, int64_t n_prefix, int64_t n_tok, void *out, const Split &sp, void *ws,
-                  hipStream_t stream, const float *qscale = nullptr) {
+                  hipStream_t stream, const float *qscale = nullptr, const float *rope = nullptr) {
     AttnParams p;
     fill_common(p, d);
     p.q = Q; p.kn = K; p.vn = V; p.out = out;
     const bool reverse = mode == kModePrefill;
-    if (mode == kModePrefill) {
+    const bool keys_in_cache = mode == kModePrefill && rope != nullptr;
+    if (keys_in_cache) {
+        p.rope = rope;
+        p.kn = kc;
+        p.vn = vc;
+        p.new_tok_stride = d->head_dim;
+        p.new_head_stride = d->capacity * d->head_dim;
+    } else if (mode == kModePrefill) {
         p.kc_out = kc;
         p.vc_out = vc;
     } else {
@@ -172,7 +225,7 @@ int launch_single(const kvr_desc *d, int mode, const void *Q, const void *K, con
     } else if (is16(d)) {
         e = launch_attn_bf16(p, d->head_dim, mode, f16(d), (int)grid, stream);
     } else {
-        if (mode == kModePrefill) {   // the fp32 kernel does not write the cache itself
+        if (mode == kModePrefill && !keys_in_cache) {   // the fp32 kernel does not write the cache itself
             const int st = append_impl(d, K, V, n_tok, kc, vc, 0, stream);
             if (st) return st;
         }
@@ -189,6 +242,77 @@ int launch_single(const kvr_desc *d, int mode, const void *Q, const void *K, con
     return KVR_OK;
 }
 
+
+// Validation shared by both batched entry points; *total receives cu[n] and
+// *longest the longest reader.  Returns KVR_OK with *total == 0 for no work.
+int check_batched(const kvr_desc *desc, const void *Qs, const void *Ks, const void *Vs, const int32_t *cu,
+                  int32_t n, const void *kcache, const void *vcache, int64_t L_prefix, void *out,
+                  int64_t *total, int64_t *longest) {
+    *total = 0;
+    *longest = 0;
+    int st = check_desc(desc);
+    if (st) return st;
+    if (n < 0 || L_prefix < 0 || L_prefix > kMaxKeys) return KVR_ERR_SHAPE;
+    if (L_prefix > desc->capacity) return KVR_ERR_CAPACITY;
+    if (n == 0) return KVR_OK;
+    if (!cu) return KVR_ERR_NULL;
+    if (cu[0] != 0) return KVR_ERR_SHAPE;
+    for (int32_t i = 0; i < n; ++i)
+        if (cu[i + 1] < cu[i]) return KVR_ERR_SHAPE;
+    if ((int64_t)cu[n] > kMaxTokens) return KVR_ERR_SHAPE;
+    for (int32_t i = 0; i < n; ++i) {
+        const int64_t len = cu[i + 1] - cu[i];
+        if ((int64_t)(desc->n_q_heads / desc->n_kv_heads) * len > 0x7fffffff) return KVR_ERR_SHAPE;
+        if (len > *longest) *longest = len;
+    }
+    if (cu[n] == 0) return KVR_OK;
+    if (!Qs || !Ks || !Vs || !out) return KVR_ERR_NULL;
+    if (L_prefix > 0 && (!kcache || !vcache)) return KVR_ERR_NULL;
+    if (!aligned16(Qs) || !aligned16(Ks) || !aligned16(Vs) || !aligned16(out) || !aligned16(kcache) ||
+        !aligned16(vcache))
+        return KVR_ERR_ALIGN;
+    *total = cu[n];
+    return KVR_OK;
+}
+
+// rope != NULL: the query rows are rotated in registers (Ks already rotated)
+int batched_impl(const kvr_desc *desc, const void *Qs, const void *Ks, const void *Vs, const int32_t *cu,
+                 int32_t n, const void *kcache, const void *vcache, int64_t L_prefix, void *out,
+                 const float *rope, void *stream) {
+    const int64_t G = desc->n_q_heads / desc->n_kv_heads;
+    const int rpt = use_pp(desc) ? kRowsPP : rows_per_tile(desc);
+    for (int32_t first = 0; first < n; first += kMaxSegments) {
+        const int32_t cnt = (n - first) < kMaxSegments ? (n - first) : kMaxSegments;
+        AttnParams p;
+        fill_common(p, desc);
+        p.q = Qs; p.kn = Ks; p.vn = Vs; p.kc = kcache; p.vc = vcache; p.out = out;
+        p.rope = rope;
+        p.n_prefix = L_prefix;
+        p.reverse = 0;
+        int32_t tiles = 0, seg = 0;
+        for (int32_t i = 0; i < cnt; ++i) {
+            const int64_t len = cu[first + i + 1] - cu[first + i];
+            if (len == 0) continue;   // an empty reader has no rows
+            p.seg_tok0[seg] = cu[first + i];
+            p.seg_tok0[seg + 1] = cu[first + i + 1];
+            p.seg_tile0[seg] = tiles;
+            tiles += (int32_t)((G * len + rpt - 1) / rpt);
+            ++seg;
+        }
+        if (seg == 0) continue;
+        p.seg_tile0[seg] = tiles;
+        p.n_seg = seg;
+        p.tiles_total = tiles;
+        p.rows_total = 0;
+        const int64_t grid = (int64_t)tiles * p.n_kv_heads;
+        hipError_t e = use_pp(desc) ? launch_attn_pp(p, kModeReaders, f16(desc), (int)grid, (hipStream_t)stream)
+                       : is16(desc) ? launch_attn_bf16(p, desc->head_dim, kModeReaders, f16(desc), (int)grid,
+                                                       (hipStream_t)stream)
+                                    : launch_attn_f32(p, desc->head_dim, (int)grid, (hipStream_t)stream);
+        if (e != hipSuccess) return KVR_ERR_DEVICE;
+    }
+    return KVR_OK;
+}
 
 }  // namespace
 }  // namespace kvr
@@ -210,6 +334,7 @@ const char *kvr_strerror(int status) {
         case KVR_ERR_ALIGN: return "device pointer not 16-byte aligned";
         case KVR_ERR_DEVICE: return "HIP call or kernel launch failed";
         case KVR_ERR_MISMATCH: return "artifact metadata does not match the running model (model id, dtype or shape)";
+        case KVR_ERR_POSITION: return "RoPE table lacks a position the call rotates, or invalid table arguments";
         default: return "unknown kvr status";
     }
 }
@@ -311,58 +436,10 @@ int kvr_continue_batched(const kvr_desc *desc, const void *Qs, const void *Ks, c
                          const int32_t *cu, int32_t n, const void *kcache, const void *vcache,
                          int64_t L_prefix, void *out, void *ws, size_t ws_bytes, void *stream) {
     (void)ws; (void)ws_bytes;   // the batched path needs no workspace
-    int st = check_desc(desc);
-    if (st) return st;
-    if (n < 0 || L_prefix < 0 || L_prefix > kMaxKeys) return KVR_ERR_SHAPE;
-    if (L_prefix > desc->capacity) return KVR_ERR_CAPACITY;
-    if (n == 0) return KVR_OK;
-    if (!cu) return KVR_ERR_NULL;
-    if (cu[0] != 0) return KVR_ERR_SHAPE;
-    for (int32_t i = 0; i < n; ++i)
-        if (cu[i + 1] < cu[i]) return KVR_ERR_SHAPE;
-    const int64_t total = cu[n];
-    if (total > kMaxTokens) return KVR_ERR_SHAPE;
-    for (int32_t i = 0; i < n; ++i)
-        if ((int64_t)(desc->n_q_heads / desc->n_kv_heads) * (cu[i + 1] - cu[i]) > 0x7fffffff) return KVR_ERR_SHAPE;
-    if (total == 0) return KVR_OK;
-    if (!Qs || !Ks || !Vs || !out) return KVR_ERR_NULL;
-    if (L_prefix > 0 && (!kcache || !vcache)) return KVR_ERR_NULL;
-    if (!aligned16(Qs) || !aligned16(Ks) || !aligned16(Vs) || !aligned16(out) || !aligned16(kcache) ||
-        !aligned16(vcache))
-        return KVR_ERR_ALIGN;
-
-    const int64_t G = desc->n_q_heads / desc->n_kv_heads;
-    const int rpt = use_pp(desc) ? kRowsPP : rows_per_tile(desc);
-    for (int32_t first = 0; first < n; first += kMaxSegments) {
-        const int32_t cnt = (n - first) < kMaxSegments ? (n - first) : kMaxSegments;
-        AttnParams p;
-        fill_common(p, desc);
-        p.q = Qs; p.kn = Ks; p.vn = Vs; p.kc = kcache; p.vc = vcache; p.out = out;
-        p.n_prefix = L_prefix;
-        p.reverse = 0;
-        int32_t tiles = 0, seg = 0;
-        for (int32_t i = 0; i < cnt; ++i) {
-            const int64_t len = cu[first + i + 1] - cu[first + i];
-            if (len == 0) continue;   // an empty reader has no rows
-            p.seg_tok0[seg] = cu[first + i];
-            p.seg_tok0[seg + 1] = cu[first + i + 1];
-            p.seg_tile0[seg] = tiles;
-            tiles += (int32_t)((G * len + rpt - 1) / rpt);
-            ++seg;
-        }
-        if (seg == 0) continue;
-        p.seg_tile0[seg] = tiles;
-        p.n_seg = seg;
-        p.tiles_total = tiles;
-        p.rows_total = 0;
-        const int64_t grid = (int64_t)tiles * p.n_kv_heads;
-        hipError_t e = use_pp(desc) ? launch_attn_pp(p, kModeReaders, f16(desc), (int)grid, (hipStream_t)stream)
-                       : is16(desc) ? launch_attn_bf16(p, desc->head_dim, kModeReaders, f16(desc), (int)grid,
-                                                       (hipStream_t)stream)
-                                    : launch_attn_f32(p, desc->head_dim, (int)grid, (hipStream_t)stream);
-        if (e != hipSuccess) return KVR_ERR_DEVICE;
-    }
-    return KVR_OK;
+    int64_t total, longest;
+    const int st = check_batched(desc, Qs, Ks, Vs, cu, n, kcache, vcache, L_prefix, out, &total, &longest);
+    if (st || total == 0) return st;
+    return batched_impl(desc, Qs, Ks, Vs, cu, n, kcache, vcache, L_prefix, out, nullptr, stream);
 }
 
 int kvr_cache_append(const kvr_desc *desc, const void *Ks, const void *Vs, int64_t S, void *kcache,
@@ -375,6 +452,135 @@ int kvr_cache_append(const kvr_desc *desc, const void *Ks, const void *Vs, int64
     if (!Ks || !Vs || !kcache || !vcache) return KVR_ERR_NULL;
     if (!aligned16(Ks) || !aligned16(Vs) || !aligned16(kcache) || !aligned16(vcache)) return KVR_ERR_ALIGN;
     return append_impl(desc, Ks, Vs, S, kcache, vcache, L_cur, (hipStream_t)stream);
+}
+
+int kvr_rope_table(int32_t head_dim, double base, int64_t n_pos, float *cos_sin, void *stream) {
+    if (head_dim != 64 && head_dim != 128) return KVR_ERR_SHAPE;
+    if (!(base > 0.0) || isinf(base) || n_pos < 0 || n_pos > kMaxKeys) return KVR_ERR_POSITION;
+    if (n_pos == 0) return KVR_OK;
+    if (!cos_sin) return KVR_ERR_NULL;
+    if (!aligned16(cos_sin)) return KVR_ERR_ALIGN;
+    return to_status(launch_rope_table(cos_sin, head_dim, base, n_pos, (hipStream_t)stream));
+}
+
+int kvr_rope_apply(const kvr_desc *desc, const kvr_rope *rope, const void *x, int64_t n_tok, int32_t n_heads,
+                   int64_t pos0, void *y, void *stream) {
+    int st = check_desc(desc);
+    if (st) return st;
+    if (n_tok < 0 || n_tok > kMaxTokens || n_heads <= 0 || n_heads > 4096) return KVR_ERR_SHAPE;
+    if (pos0 < 0 || pos0 > kMaxKeys) return KVR_ERR_POSITION;
+    if (n_tok == 0) return KVR_OK;
+    if (!x || !y) return KVR_ERR_NULL;
+    if ((st = check_rope(rope, pos0 + n_tok))) return st;
+    if (!aligned16(x) || !aligned16(y)) return KVR_ERR_ALIGN;
+    RopeParams rp = rope_params(desc, rope, n_tok, pos0);
+    rp.n_jobs = 1;
+    rp.job[0].x = x;
+    rp.job[0].y = y;
+    rp.job[0].n_heads = n_heads;
+    return to_status(launch_rope(rp, desc->head_dim, desc->dtype, (hipStream_t)stream));
+}
+
+int kvr_prefill_rope(const kvr_desc *desc, const kvr_rope *rope, const void *Q, const void *K, const void *V,
+                     int64_t L, void *out, void *kcache, void *vcache, void *stream) {
+    int st = check_desc(desc);
+    if (st) return st;
+    if (L < 0 || L > kMaxTokens) return KVR_ERR_SHAPE;
+    if (L > desc->capacity) return KVR_ERR_CAPACITY;
+    if (L == 0) return KVR_OK;
+    if (!Q || !K || !V || !out || !kcache || !vcache) return KVR_ERR_NULL;
+    if ((st = check_rope(rope, L))) return st;
+    if (!aligned16(Q) || !aligned16(K) || !aligned16(V) || !aligned16(out) || !aligned16(kcache) ||
+        !aligned16(vcache))
+        return KVR_ERR_ALIGN;
+    // rotated keys and the values into cache rows [0, L), then attention over them
+    RopeParams rp = rope_params(desc, rope, L, 0);
+    rp.n_jobs = 1;
+    rp.job[0].x = K;
+    rp.job[0].cache = kcache;
+    rp.job[0].v = V;
+    rp.job[0].vcache = vcache;
+    rp.job[0].n_heads = desc->n_kv_heads;
+    if (launch_rope(rp, desc->head_dim, desc->dtype, (hipStream_t)stream) != hipSuccess) return KVR_ERR_DEVICE;
+    Split none{1, 0, 0};
+    return launch_single(desc, kModePrefill, Q, nullptr, nullptr, kcache, vcache, 0, L, out, none, nullptr,
+                         (hipStream_t)stream, nullptr, rope->cos_sin);
+}
+
+size_t kvr_workspace_bytes_rope(const kvr_desc *desc, int64_t L_prefix, int64_t total_S, int32_t n) {
+    if (check_desc(desc) != KVR_OK || L_prefix < 0 || total_S < 0 || n < 0) return (size_t)-1;
+    return rope_ws(desc, L_prefix, total_S, n).total;
+}
+
+int kvr_continue_rope(const kvr_desc *desc, const kvr_rope *rope, const void *Qs, const void *Ks, const void *Vs,
+                      void *kcache, void *vcache, int64_t L_prefix, int64_t S, int32_t append, void *out, void *ws,
+                      size_t ws_bytes, void *stream) {
+    int st = check_desc(desc);
+    if (st) return st;
+    if (L_prefix < 0 || S < 0 || S > kMaxTokens || L_prefix > kMaxKeys) return KVR_ERR_SHAPE;
+    if (L_prefix > desc->capacity) return KVR_ERR_CAPACITY;
+    if (append && L_prefix + S > desc->capacity) return KVR_ERR_CAPACITY;
+    if (S == 0) return KVR_OK;
+    if (!Qs || !Ks || !Vs || !out || !ws) return KVR_ERR_NULL;
+    if ((L_prefix > 0 || append) && (!kcache || !vcache)) return KVR_ERR_NULL;
+    if ((st = check_rope(rope, L_prefix + S))) return st;
+    const RopeWs w = rope_ws(desc, L_prefix, S, 1);
+    if (ws_bytes < w.total) return KVR_ERR_WORKSPACE;
+    if (!aligned16(Qs) || !aligned16(Ks) || !aligned16(Vs) || !aligned16(out) || !aligned16(kcache) ||
+        !aligned16(vcache) || !aligned16(ws))
+        return KVR_ERR_ALIGN;
+    unsigned char *wsb = (unsigned char *)ws;
+    // the rows at positions L_prefix..: queries and keys rotated into the
+    // workspace, and with append the rotated keys and the values into the cache
+    RopeParams rp = rope_params(desc, rope, S, L_prefix);
+    rp.n_jobs = 2;
+    rp.job[0].x = Qs;
+    rp.job[0].y = wsb + w.q_off;
+    rp.job[0].n_heads = desc->n_q_heads;
+    rp.job[1].x = Ks;
+    rp.job[1].y = wsb + w.k_off;
+    rp.job[1].n_heads = desc->n_kv_heads;
+    if (append) {
+        rp.job[1].cache = kcache;
+        rp.job[1].v = Vs;
+        rp.job[1].vcache = vcache;
+    }
+    if (launch_rope(rp, desc->head_dim, desc->dtype, (hipStream_t)stream) != hipSuccess) return KVR_ERR_DEVICE;
+    const Split sp = plan_split(desc, L_prefix, S);
+    return launch_single(desc, kModeContinue, wsb + w.q_off, wsb + w.k_off, Vs, kcache, vcache, L_prefix, S, out,
+                         sp, ws, (hipStream_t)stream);
+}
+
+int kvr_continue_batched_rope(const kvr_desc *desc, const kvr_rope *rope, const void *Qs, const void *Ks,
+                              const void *Vs, const int32_t *cu, int32_t n, const void *kcache, const void *vcache,
+                              int64_t L_prefix, void *out, void *ws, size_t ws_bytes, void *stream) {
+    int64_t total, longest;
+    int st = check_batched(desc, Qs, Ks, Vs, cu, n, kcache, vcache, L_prefix, out, &total, &longest);
+    if (st || total == 0) return st;
+    if ((st = check_rope(rope, L_prefix + longest))) return st;
+    const RopeWs w = rope_ws(desc, L_prefix, total, n < 2 ? 2 : n);
+    if (!ws) return KVR_ERR_NULL;
+    if (ws_bytes < w.total) return KVR_ERR_WORKSPACE;
+    if (!aligned16(ws)) return KVR_ERR_ALIGN;
+    // each reader's keys rotated at L_prefix + (row within the reader), in
+    // groups of at most kMaxSegments readers (the pre-pass's segment table)
+    const size_t row_b = (size_t)desc->n_kv_heads * desc->head_dim * elt_bytes(desc);
+    unsigned char *kr = (unsigned char *)ws + w.k_off;
+    for (int32_t first = 0; first < n; first += kMaxSegments) {
+        const int32_t cnt = (n - first) < kMaxSegments ? (n - first) : kMaxSegments;
+        const int64_t t0 = cu[first];
+        const int64_t nt = cu[first + cnt] - t0;
+        if (nt == 0) continue;
+        RopeParams rp = rope_params(desc, rope, nt, L_prefix);
+        rp.n_seg = cnt;
+        for (int32_t i = 0; i <= cnt; ++i) rp.seg_tok0[i] = (int32_t)(cu[first + i] - t0);
+        rp.n_jobs = 1;
+        rp.job[0].x = (const unsigned char *)Ks + (size_t)t0 * row_b;
+        rp.job[0].y = kr + (size_t)t0 * row_b;
+        rp.job[0].n_heads = desc->n_kv_heads;
+        if (launch_rope(rp, desc->head_dim, desc->dtype, (hipStream_t)stream) != hipSuccess) return KVR_ERR_DEVICE;
+    }
+    return batched_impl(desc, Qs, kr, Vs, cu, n, kcache, vcache, L_prefix, out, rope->cos_sin, stream);
 }
 
 }  // extern "C"

@@ -25,6 +25,15 @@ struct AttnParams {
     void *vc_out;
     float *ws;       // split partials: O [nsplit][Hkv][rows][D], then (m, l) [nsplit][Hkv][rows][2]
     const float *qscale;   // int8 artifact continuation: {s_K, s_V} (kc/vc then point at the codes)
+    // RoPE table [pos][D/2] of (cos, sin), or null.  Set for prefill and many
+    // readers only: those kernels rotate each query row in registers at its
+    // position n_prefix + token (continuations get their rows rotated by the
+    // pre-pass instead).
+    const float *rope;
+    // Element strides of kn/vn: token and kv head.  Token-major new rows have
+    // (n_kv_heads * D, D); prefill with RoPE reads its rotated rows back from
+    // the cache, (D, cap * D).  Honoured by the prefill / readers kernels.
+    int64_t new_tok_stride, new_head_stride;
     int64_t cap;
     int64_t n_prefix;  // cached keys, positions [0, n_prefix); every query row sees them all
     int64_t chunk;     // prefix keys per split, a multiple of the key tile
@@ -89,6 +98,30 @@ hipError_t launch_quantize(const QuantParams &p, hipStream_t s);
 hipError_t launch_attn_f32(const AttnParams &p, int head_dim, int grid, hipStream_t s);
 // cache write
 hipError_t launch_append(const AppendParams &p, hipStream_t s);
+
+// RoPE pre-pass: rotate token-major rows [n_tok][n_heads][D] at their
+// positions into token-major rows (y) and/or cache rows (cache, row = the
+// position), and copy value rows into a cache unchanged.
+struct RopeJob {
+    const void *x;       // rows to rotate, [n_tok][n_heads][D]
+    void *y;             // rotated rows, token-major (may equal x), or null
+    void *cache;         // rotated rows into [n_heads][cap][D] at row = position, or null
+    const void *v;       // rows copied unrotated into vcache at row = position, or null
+    void *vcache;
+    int32_t n_heads;
+};
+struct RopeParams {
+    RopeJob job[2];
+    const float *cs;     // [n_pos][D/2] (cos, sin)
+    int64_t n_tok, cap;
+    int64_t pos0;        // token t of segment s sits at pos0 + t - seg_tok0[s]
+    int32_t n_jobs;
+    int32_t n_seg;
+    int32_t seg_tok0[kMaxSegments + 1];
+};
+// elt: 0 bf16, 1 fp32, 2 fp16 (kvr_dtype)
+hipError_t launch_rope(const RopeParams &p, int head_dim, int elt, hipStream_t s);
+hipError_t launch_rope_table(float *cs, int head_dim, double base, int64_t n_pos, hipStream_t s);
 
 // row-tile geometry of the two paths
 constexpr int kRowsBf16 = 128;  // query rows per workgroup, bf16 path

@@ -17,14 +17,16 @@ LIB_PATH = os.path.join(_PKG, "libkvr.so")
 
 KVR_OK, KVR_ERR_NULL, KVR_ERR_SHAPE, KVR_ERR_DTYPE = 0, 1, 2, 3
 KVR_ERR_CAPACITY, KVR_ERR_WORKSPACE, KVR_ERR_ALIGN, KVR_ERR_DEVICE = 4, 5, 6, 7
-KVR_ERR_MISMATCH = 8
+KVR_ERR_MISMATCH, KVR_ERR_POSITION = 8, 9
 KVR_ARTIFACT_HEADER_BYTES = 256
 KVR_BF16, KVR_F32, KVR_F16 = 0, 1, 2
 
 EXPORTS = ("kvr_prefill", "kvr_continue", "kvr_continue_batched", "kvr_cache_append",
            "kvr_workspace_bytes", "kvr_strerror", "kvr_abi_version",
            "kvr_q8_bytes", "kvr_quantize_cache", "kvr_continue_q8",
-           "kvr_artifact_bytes", "kvr_artifact_save", "kvr_artifact_load")
+           "kvr_artifact_bytes", "kvr_artifact_save", "kvr_artifact_load",
+           "kvr_rope_table", "kvr_rope_apply", "kvr_prefill_rope", "kvr_continue_rope",
+           "kvr_continue_batched_rope", "kvr_workspace_bytes_rope")
 
 _TORCH_DTYPE = {KVR_BF16: torch.bfloat16, KVR_F32: torch.float32, KVR_F16: torch.float16}
 
@@ -34,6 +36,10 @@ class kvr_desc(ctypes.Structure):
                 ("head_dim", ctypes.c_int32), ("dtype", ctypes.c_int32),
                 ("scale", ctypes.c_float), ("reserved", ctypes.c_int32),
                 ("capacity", ctypes.c_int64)]
+
+
+class kvr_rope(ctypes.Structure):
+    _fields_ = [("cos_sin", ctypes.c_void_p), ("n_pos", ctypes.c_int64)]
 
 
 class KvrError(RuntimeError):
@@ -73,12 +79,22 @@ def load():
     lib.kvr_artifact_save.argtypes = [D, ctypes.c_char_p, ctypes.c_int32, I64, PP, PP, P, SZ, P]
     lib.kvr_artifact_load.argtypes = [D, ctypes.c_char_p, ctypes.c_int32, P, SZ, PP, PP,
                                       ctypes.POINTER(ctypes.c_int64), P]
+    R = ctypes.POINTER(kvr_rope)
+    lib.kvr_rope_table.argtypes = [ctypes.c_int32, ctypes.c_double, I64, P, P]
+    lib.kvr_rope_apply.argtypes = [D, R, P, I64, ctypes.c_int32, I64, P, P]
+    lib.kvr_prefill_rope.argtypes = [D, R, P, P, P, I64, P, P, P, P]
+    lib.kvr_continue_rope.argtypes = [D, R, P, P, P, P, P, I64, I64, ctypes.c_int32, P, P, SZ, P]
+    lib.kvr_continue_batched_rope.argtypes = [D, R, P, P, P, ctypes.POINTER(ctypes.c_int32), ctypes.c_int32,
+                                              P, P, I64, P, P, SZ, P]
+    lib.kvr_workspace_bytes_rope.argtypes = [D, I64, I64, ctypes.c_int32]
+    lib.kvr_workspace_bytes_rope.restype = SZ
     lib.kvr_strerror.argtypes = [ctypes.c_int]
     lib.kvr_strerror.restype = ctypes.c_char_p
     lib.kvr_abi_version.argtypes = []
     for f in (lib.kvr_prefill, lib.kvr_continue, lib.kvr_continue_batched, lib.kvr_cache_append,
               lib.kvr_abi_version, lib.kvr_quantize_cache, lib.kvr_continue_q8, lib.kvr_artifact_save,
-              lib.kvr_artifact_load):
+              lib.kvr_artifact_load, lib.kvr_rope_table, lib.kvr_rope_apply, lib.kvr_prefill_rope,
+              lib.kvr_continue_rope, lib.kvr_continue_batched_rope):
         f.restype = ctypes.c_int
     _lib = lib
     return lib
@@ -298,3 +314,104 @@ def workspace_for(desc, L_prefix, total_S, n=1, device="cuda"):
     if nb == 0:
         return None
     return torch.empty(nb, dtype=torch.uint8, device=device)
+
+
+# ---------------------------------------------------------------- RoPE
+QWEN3_ROPE_BASE = 1.0e6
+
+
+class RopeTable:
+    """A device cos/sin table (float [n_pos][head_dim/2][2], torch-allocated)
+    filled by kvr_rope_table; pass it to the *_rope entry points."""
+
+    def __init__(self, head_dim, n_pos, base=QWEN3_ROPE_BASE, device="cuda", stream=None):
+        self.head_dim, self.n_pos, self.base = int(head_dim), int(n_pos), float(base)
+        self.cos_sin = torch.empty((max(self.n_pos, 1), self.head_dim // 2, 2), dtype=torch.float32, device=device)
+        kvr_rope_table(self.head_dim, self.base, self.n_pos, self.cos_sin, stream)
+
+    def c(self):
+        return kvr_rope(self.cos_sin.data_ptr(), self.n_pos)
+
+
+def kvr_rope_table(head_dim, base, n_pos, cos_sin, stream=None):
+    if (not isinstance(cos_sin, torch.Tensor) or not cos_sin.is_cuda or cos_sin.dtype != torch.float32
+            or not cos_sin.is_contiguous() or cos_sin.numel() < int(n_pos) * int(head_dim)):
+        raise ValueError("cos_sin must be a contiguous float32 GPU tensor of n_pos * head_dim values")
+    _raise(load().kvr_rope_table(int(head_dim), float(base), int(n_pos), cos_sin.data_ptr(), _stream(stream)),
+           "kvr_rope_table")
+
+
+def _rope(rope, desc):
+    if not isinstance(rope, RopeTable):
+        raise ValueError("rope must be a RopeTable")
+    if rope.head_dim != desc.head_dim:
+        raise ValueError("RoPE table head_dim %d, descriptor %d" % (rope.head_dim, desc.head_dim))
+    return ctypes.byref(rope.c())
+
+
+def kvr_rope_apply(desc, rope, x, pos0, y=None, stream=None):
+    """Rotate rows x [n_tok, n_heads, head_dim] at positions pos0.. into y (default: in place)."""
+    if x.dim() != 3:
+        raise ValueError("x must be [n_tok, n_heads, head_dim]")
+    n_tok, n_heads = x.shape[0], x.shape[1]
+    y = x if y is None else y
+    xp = _check(x, "x", desc, (n_tok, n_heads, desc.head_dim))
+    yp = _check(y, "y", desc, (n_tok, n_heads, desc.head_dim))
+    _raise(load().kvr_rope_apply(ctypes.byref(desc), _rope(rope, desc), xp, int(n_tok), int(n_heads), int(pos0),
+                                 yp, _stream(stream)), "kvr_rope_apply")
+    return y
+
+
+def kvr_prefill_rope(desc, rope, Q, K, V, L, out, kcache, vcache, stream=None):
+    Hq, Hkv, d = desc.n_q_heads, desc.n_kv_heads, desc.head_dim
+    q = _check(Q, "Q", desc, (L, Hq, d))
+    k = _check(K, "K", desc, (L, Hkv, d))
+    v = _check(V, "V", desc, (L, Hkv, d))
+    o = _check(out, "out", desc, (L, Hq, d))
+    kc, vc = _cache_ptrs(desc, kcache, vcache, True)
+    _raise(load().kvr_prefill_rope(ctypes.byref(desc), _rope(rope, desc), q, k, v, int(L), o, kc, vc,
+                                   _stream(stream)), "kvr_prefill_rope")
+
+
+def kvr_workspace_bytes_rope(desc, L_prefix, total_S, n=1):
+    return load().kvr_workspace_bytes_rope(ctypes.byref(desc), int(L_prefix), int(total_S), int(n))
+
+
+def workspace_for_rope(desc, L_prefix, total_S, n=1, device="cuda"):
+    """Allocate (with torch) the workspace of a RoPE continuation."""
+    nb = kvr_workspace_bytes_rope(desc, L_prefix, total_S, n)
+    if nb == ctypes.c_size_t(-1).value:
+        raise ValueError("invalid layer descriptor")
+    return torch.empty(max(nb, 1), dtype=torch.uint8, device=device)
+
+
+def kvr_continue_rope(desc, rope, Qs, Ks, Vs, kcache, vcache, L_prefix, S, out, ws, append=False, stream=None):
+    Hq, Hkv, d = desc.n_q_heads, desc.n_kv_heads, desc.head_dim
+    q = _check(Qs, "Qs", desc, (S, Hq, d))
+    k = _check(Ks, "Ks", desc, (S, Hkv, d))
+    v = _check(Vs, "Vs", desc, (S, Hkv, d))
+    o = _check(out, "out", desc, (S, Hq, d))
+    kc, vc = _cache_ptrs(desc, kcache, vcache, L_prefix > 0 or append)
+    wp, wn = _workspace(ws)
+    _raise(load().kvr_continue_rope(ctypes.byref(desc), _rope(rope, desc), q, k, v, kc, vc, int(L_prefix), int(S),
+                                    1 if append else 0, o, wp, wn, _stream(stream)), "kvr_continue_rope")
+
+
+def kvr_continue_batched_rope(desc, rope, Qs, Ks, Vs, cu_seqlens, kcache, vcache, L_prefix, out, ws,
+                              stream=None):
+    Hq, Hkv, d = desc.n_q_heads, desc.n_kv_heads, desc.head_dim
+    cu = [int(x) for x in (cu_seqlens.tolist() if isinstance(cu_seqlens, torch.Tensor) else cu_seqlens)]
+    n = len(cu) - 1
+    if n < 0:
+        raise ValueError("cu_seqlens needs at least one entry")
+    total = cu[-1]
+    q = _check(Qs, "Qs", desc, (total, Hq, d))
+    k = _check(Ks, "Ks", desc, (total, Hkv, d))
+    v = _check(Vs, "Vs", desc, (total, Hkv, d))
+    o = _check(out, "out", desc, (total, Hq, d))
+    kc, vc = _cache_ptrs(desc, kcache, vcache, L_prefix > 0)
+    arr = (ctypes.c_int32 * len(cu))(*cu)
+    wp, wn = _workspace(ws)
+    _raise(load().kvr_continue_batched_rope(ctypes.byref(desc), _rope(rope, desc), q, k, v, arr, n, kc, vc,
+                                            int(L_prefix), o, wp, wn, _stream(stream)),
+           "kvr_continue_batched_rope")

@@ -70,8 +70,8 @@ def test_exports_match_header(lib):
 
 
 def test_abi_version_and_strerror(lib):
-    assert lib.kvr_abi_version() == 2
-    for code in range(9):
+    assert lib.kvr_abi_version() == 3
+    for code in range(10):
         assert len(lib.kvr_strerror(code)) > 0
     assert b"unknown" in lib.kvr_strerror(99)
 
