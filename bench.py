@@ -43,6 +43,7 @@ def parse():
     ap.add_argument("--no-decode36", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-artifact", action="store_true")
+    ap.add_argument("--no-rope", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="target CPU-oracle sample time")
     ap.add_argument("--sweep-lengths", type=str, default=None,
                     help="comma-separated prefix lengths for the sweep (default: all four)")
@@ -233,6 +234,8 @@ def main():
         result["decode36"] = decode36(torch, kvr, A, W, dev, stream)
     if not args.no_artifact:
         result["artifact"] = artifact(torch, kvr, W, dev, stream)
+    if not args.no_rope:
+        result["rope"] = rope_calls(torch, kvr, A, W, dev, stream)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(q, k, v, A, args.cpu_seconds)
     print(json.dumps(result), flush=True)
@@ -492,6 +495,77 @@ def artifact(torch, kvr, W, dev, stream):
     del kcs, vcs, k2, v2, host
     torch.cuda.empty_cache()
     return res
+
+
+def rope_calls(torch, kvr, A, W, dev, stream):
+    """The step's calls with fused RoPE (positions 0.. for the prefill, L.. for
+    the continuations) next to the same calls without it, alternated in blocks
+    so that both see the same clock."""
+    sh = W.QWEN
+    Hq, Hkv, D = sh.n_q_heads, sh.n_kv_heads, sh.head_dim
+    L, S = W.LAYER_L, W.LAYER_S
+    n = L + S
+    q, k, v = (x.to(dev) for x in W.qkv(n, sh, seed=0))
+    desc = kvr.make_desc(Hq, Hkv, D, torch.bfloat16, n + 1)
+    lens = W.reader_lengths()
+    cu = W.cu_seqlens(lens)
+    tab = kvr.RopeTable(D, n + 1 + max(lens))
+    kc, vc = (torch.zeros((Hkv, n + 1, D), dtype=torch.bfloat16, device=dev) for _ in range(2))
+    kc2, vc2 = torch.zeros_like(kc), torch.zeros_like(vc)
+    out, out_r = torch.empty_like(q), torch.empty_like(q)
+    qs, ks, vs = q[L:].contiguous(), k[L:].contiguous(), v[L:].contiguous()
+    oc, oc_r = torch.empty_like(qs), torch.empty_like(qs)
+    ws, ws_r = kvr.workspace_for(desc, L, S), kvr.workspace_for_rope(desc, L, S)
+    rq, rk, rv = (x.to(dev) for x in W.qkv(cu[-1], sh, seed=1))
+    ro = torch.empty_like(rq)
+    ws_rd = kvr.workspace_for_rope(desc, L, cu[-1], len(lens))
+    dq, dk, dv = (x.to(dev) for x in W.qkv(1, sh, seed=2))
+    do = torch.empty_like(dq)
+    ws_d, ws_dr = kvr.workspace_for(desc, n, 1), kvr.workspace_for_rope(desc, n, 1)
+    calls = {
+        "prefill": (lambda: kvr.kvr_prefill(desc, q, k, v, n, out, kc, vc),
+                    lambda: kvr.kvr_prefill_rope(desc, tab, q, k, v, n, out_r, kc2, vc2)),
+        "continue": (lambda: kvr.kvr_continue(desc, qs, ks, vs, kc, vc, L, S, oc, ws),
+                     lambda: kvr.kvr_continue_rope(desc, tab, qs, ks, vs, kc2, vc2, L, S, oc_r, ws_r)),
+        "readers": (lambda: kvr.kvr_continue_batched(desc, rq, rk, rv, cu, kc, vc, L, ro),
+                    lambda: kvr.kvr_continue_batched_rope(desc, tab, rq, rk, rv, cu, kc2, vc2, L, ro, ws_rd)),
+        "decode_step": (lambda: (kvr.kvr_continue(desc, dq, dk, dv, kc, vc, n, 1, do, ws_d),
+                                 kvr.kvr_cache_append(desc, dk, dv, 1, kc, vc, n)),
+                        lambda: kvr.kvr_continue_rope(desc, tab, dq, dk, dv, kc2, vc2, n, 1, do, ws_dr,
+                                                      append=True)),
+    }
+    res = {}
+    for name, (plain, roped) in calls.items():
+        for f in (plain, roped):          # warm the clock up
+            t_end = time.perf_counter() + 0.1
+            while time.perf_counter() < t_end:
+                f()
+                torch.cuda.synchronize()
+        tp, tr = [], []
+        for _ in range(4):
+            tp += timed(torch, stream, lambda i: plain(), 10)
+            tr += timed(torch, stream, lambda i: roped(), 10)
+        res[name] = (sorted(tp)[len(tp) // 2], sorted(tr)[len(tr) // 2])
+    kvr.kvr_prefill_rope(desc, tab, q, k, v, n, out_r, kc2, vc2)
+    kvr.kvr_continue_rope(desc, tab, qs, ks, vs, kc2, vc2, L, S, oc_r, ws_r)
+    torch.cuda.synchronize()
+    pf = A.prefill_flops(n, Hq, D)
+    rd = A.batched_flops(L, lens, Hq, D)
+    r = {
+        "what": "the layer step's calls with RoPE fused (rotation at positions 0.. / L..; base 1e6) next to "
+                "the same calls without; medians of 40 timed calls each",
+        "prefill_ms": [round(res["prefill"][0] * 1e3, 4), round(res["prefill"][1] * 1e3, 4)],
+        "prefill_tflops": [round(pf / res["prefill"][0] / 1e12, 1), round(pf / res["prefill"][1] / 1e12, 1)],
+        "continue_us": [round(res["continue"][0] * 1e6, 2), round(res["continue"][1] * 1e6, 2)],
+        "readers_ms": [round(res["readers"][0] * 1e3, 4), round(res["readers"][1] * 1e3, 4)],
+        "readers_tflops": [round(rd / res["readers"][0] / 1e12, 1), round(rd / res["readers"][1] / 1e12, 1)],
+        "decode_step_us": [round(res["decode_step"][0] * 1e6, 2), round(res["decode_step"][1] * 1e6, 2)],
+        "pairs": "[without RoPE, with RoPE]",
+        "claim1_maxabs": float((oc_r - out_r[L:]).abs().max()),
+    }
+    del q, k, v, kc, vc, kc2, vc2, out, out_r, rq, rk, rv, ro
+    torch.cuda.empty_cache()
+    return r
 
 
 def cpu_baseline(q, k, v, A, target_s):
