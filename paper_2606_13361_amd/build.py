@@ -13,6 +13,9 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libkvr.so")
+# the decoder layer around the attention: its own library, linked against
+# libkvr's public ABI and hipBLASLt
+MODEL_LIB = os.path.join(PKG, "libkvr_model.so")
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
@@ -35,10 +38,22 @@ def sources():
     return sorted(glob.glob(os.path.join(CSRC, "*.hip")))
 
 
+def model_sources():
+    return sorted(glob.glob(os.path.join(CSRC, "model", "*.hip")))
+
+
 def build(verbose=False):
-    """Always recompile; write libkvr.so atomically."""
-    tmp = LIB + ".tmp%d" % os.getpid()
-    cmd = [hipcc()] + HIPCC_FLAGS + ["-I" + INCLUDE, "-I" + CSRC] + sources() + ["-o", tmp]
+    """Always recompile both libraries."""
+    _build_one(LIB, sources(), [], verbose)
+    _build_one(MODEL_LIB, model_sources(),
+               ["-L" + PKG, "-lkvr", "-Wl,-rpath,$ORIGIN", "-L/opt/rocm/lib", "-lhipblaslt"], verbose)
+    return LIB
+
+
+def _build_one(lib, srcs, link, verbose):
+    """Compile srcs into lib, written atomically."""
+    tmp = lib + ".tmp%d" % os.getpid()
+    cmd = [hipcc()] + HIPCC_FLAGS + ["-I" + INCLUDE, "-I" + CSRC] + srcs + ["-o", tmp] + link
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)
@@ -50,8 +65,8 @@ def build(verbose=False):
         raise RuntimeError("hipcc failed:\n" + "\n".join(msgs))
     if msgs and verbose:
         print("\n".join(msgs), file=sys.stderr)
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, lib)
+    return lib
 
 
 if __name__ == "__main__":
