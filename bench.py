@@ -44,6 +44,9 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-artifact", action="store_true")
     ap.add_argument("--no-rope", action="store_true")
+    ap.add_argument("--no-model", action="store_true",
+                    help="skip the random-weight 36-layer model (Table 1's prefill vs continuation step)")
+    ap.add_argument("--model-only", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="target CPU-oracle sample time")
     ap.add_argument("--sweep-lengths", type=str, default=None,
                     help="comma-separated prefix lengths for the sweep (default: all four)")
@@ -127,6 +130,10 @@ def main():
         rec(5)
         kvr.kvr_cache_append(desc, dk, dv, 1, kc, vc, n)
         rec(6)
+
+    if args.model_only:
+        print(json.dumps({"model": model_table1(torch, A, W, dev)}), flush=True)
+        return
 
     if args.sweep_only:
         res = {"sweep": sweep(torch, kvr, A, W, dev, stream,
@@ -236,6 +243,8 @@ def main():
         result["artifact"] = artifact(torch, kvr, W, dev, stream)
     if not args.no_rope:
         result["rope"] = rope_calls(torch, kvr, A, W, dev, stream)
+    if not args.no_model:
+        result["model"] = model_table1(torch, A, W, dev)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(q, k, v, A, args.cpu_seconds)
     print(json.dumps(result), flush=True)
@@ -566,6 +575,98 @@ def rope_calls(torch, kvr, A, W, dev, stream):
     del q, k, v, kc, vc, kc2, vc2, out, out_r, rq, rk, rv, ro
     torch.cuda.empty_cache()
     return r
+
+
+TABLE1 = os.path.join(ROOT, "tests", "golden", "table1_qwen3_4b_m1pro.txt")
+
+
+def model_table1(torch, A, W, dev, lengths=(255, 485, 945, 1888, 3774)):
+    """The paper's Table 1 on this GPU with a random-weight Qwen3-4B-shaped
+    model (36 layers, hidden 2560, MLP 9728, 32/8 heads of 128, tied 151936-row
+    output embedding, bf16): a full prefill of the L-token context (the last
+    row's logits included) against ONE continuation step of one token over the
+    resident caches (its logits included)."""
+    from paper_2606_13361_amd import kvr_model as M
+    cfg = dict(M.QWEN3_4B)
+    H = cfg["hidden"]
+    Lmax = max(lengths)
+    m = M.Model(cfg, cfg["layers"], Lmax + 1, seed=0, vocab=cfg["vocab"], max_tokens=Lmax, device=dev)
+    g = torch.Generator(device=dev)
+    g.manual_seed(3)
+    h_all = torch.randn((Lmax + 1, H), generator=g, device=dev).to(torch.bfloat16)
+    paper = {}
+    for ln in open(TABLE1):
+        if ln.strip() and not ln.startswith("#"):
+            t, pf, rs, _, sp = ln.split()
+            paper[int(t)] = (float(pf), float(rs), float(sp))
+    layer_params = (H * (cfg["n_q_heads"] + 2 * cfg["n_kv_heads"]) * cfg["head_dim"]
+                    + cfg["n_q_heads"] * cfg["head_dim"] * H + 3 * H * cfg["intermediate"])
+    weight_bytes = 2 * (cfg["layers"] * layer_params + cfg["vocab"] * H)
+    rows = []
+    cur = torch.cuda.current_stream()
+    for L in lengths:
+        hp = torch.empty((L, H), dtype=torch.bfloat16, device=dev)
+        h1 = torch.empty((1, H), dtype=torch.bfloat16, device=dev)
+
+        def prefill():
+            hp.copy_(h_all[:L])
+            m.forward(hp, 0)
+            m.logits(hp)
+
+        def step():
+            h1.copy_(h_all[L:L + 1])
+            m.forward(h1, L)
+            m.logits(h1)
+
+        for _ in range(2):
+            prefill()
+        torch.cuda.synchronize()
+        tp = timed(torch, cur, lambda i: prefill(), 5)
+        for _ in range(5):
+            step()
+        torch.cuda.synchronize()
+        ts = timed(torch, cur, lambda i: step(), 20)
+        # the same step replayed from a HIP graph (no host launch cost)
+        side = torch.cuda.Stream()
+        side.wait_stream(cur)
+        with torch.cuda.stream(side):
+            step()
+        cur.wait_stream(side)
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            step()
+        graph.replay()
+        torch.cuda.synchronize()
+        tg = timed(torch, cur, lambda i: graph.replay(), 20)
+        del graph
+        t_p, t_s, t_g = sorted(tp)[len(tp) // 2], sorted(ts)[len(ts) // 2], sorted(tg)[len(tg) // 2]
+        flops = (2 * L * layer_params * cfg["layers"] + 2 * H * cfg["vocab"]
+                 + cfg["layers"] * A.prefill_flops(L, cfg["n_q_heads"], cfg["head_dim"]))
+        step_bytes = weight_bytes + cfg["layers"] * A.kv_bytes_per_token(cfg["n_kv_heads"], cfg["head_dim"], 2) * (L + 1)
+        pp = paper.get(L)
+        rows.append({
+            "tokens": L,
+            "prefill_ms": round(t_p * 1e3, 3), "prefill_tflops": round(flops / t_p / 1e12, 1),
+            "step_ms": round(t_s * 1e3, 3), "step_graph_ms": round(t_g * 1e3, 3),
+            "step_graph_GBps": round(step_bytes / t_g / 1e9, 1),
+            "speedup": round(t_p / t_g, 2),
+            "paper_prefill_s": pp[0] if pp else None, "paper_step_s": pp[1] if pp else None,
+            "paper_speedup": pp[2] if pp else None,
+        })
+    res = {
+        "what": "random-weight Qwen3-4B-shaped model, bf16, 36 layers (RMSNorm, QKV / O / gate-up / down "
+                "products on hipBLASLt, q/k norm + RoPE, this library's attention), tied 151936-row output "
+                "embedding: full prefill of the context (last row's logits) vs one continuation step of one "
+                "token over the resident caches (its logits); medians of 5 prefills and 20 steps",
+        "weights_GB": round(weight_bytes / 1e9, 3),
+        "rows": rows,
+        "paper_context": "paper Table 1: Qwen3-4B fp16 on Apple M1 Pro (MPS), speedup 8.6-49.7x; the speedup "
+                         "here uses the graph-replayed step",
+    }
+    del m, h_all
+    torch.cuda.empty_cache()
+    return res
 
 
 def cpu_baseline(q, k, v, A, target_s):
