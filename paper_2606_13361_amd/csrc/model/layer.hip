@@ -1,8 +1,8 @@
 // layer.hip -- libkvr_model: the decoder layer around libkvr's attention
 // (include/kvr_model.h).  Normalizations, the per-head q/k normalization with
-// the rotary embedding, and the gated activation are kernels of this file;
-// the four matrix products per layer go to hipBLASLt; the attention is
-// libkvr's public entry points.
+// the rotary embedding, the gated activation and the one-row products of a
+// one-token step are kernels of this file; the matrix products of more rows
+// go to hipBLASLt; the attention is libkvr's public entry points.
 #include <hipblaslt/hipblaslt.h>
 #include <math.h>
 #include <string.h>
@@ -148,6 +148,154 @@ __global__ __launch_bounds__(NT) void silu_mul_kernel(const uint16_t *gu, uint16
     }
 }
 
+// ---------------------------------------------------------------- one row
+// y[n] = sum_k x'[k] w[n][k] (+ y[n]) for a single row x: the weights are
+// streamed once from HBM, 16-byte loads coalesced along k, which bounds the
+// one-token step; a matrix-core product has nothing to reuse here.  x' is
+// built once per workgroup in LDS by the prologue:
+//   kPlain  x' = x
+//   kNorm   x' = round(rmsnorm(x) * ln)           (the layer's input norms)
+//   kSilu   x' = round(silu(x[k]) * x[K + k])     (x = the gate|up row)
+// so the norm and the activation need no launch of their own.
+enum { kPlain = 0, kNorm = 1, kSilu = 2 };
+constexpr int kGemvMaxK = 16384;
+
+struct GemvParams {
+    const uint16_t *x;     // [K] (kSilu: [2K])
+    const uint16_t *w;     // [N][K]
+    const uint16_t *ln;    // [K] (kNorm)
+    uint16_t *y;           // [N]
+    int64_t N;
+    int32_t K;
+    int32_t beta;          // 1: add into y
+    float eps;
+};
+
+constexpr int GT = 512;            // threads of a one-row-product workgroup
+constexpr int kGemvMaxGrid = 512;  // workgroups: two per compute unit
+
+template <class E, int PRO, int RW>
+__global__ __launch_bounds__(GT) void gemv_kernel(const GemvParams p) {
+    __shared__ __attribute__((aligned(16))) uint16_t xs[kGemvMaxK];
+    __shared__ float red[GT / 64];
+    constexpr int U = RW == 1 ? 8 : 4;                   // k-steps per block of loads
+    constexpr int NW = GT / 64;
+    const int tid = threadIdx.x;
+    const int KC = p.K / 8;
+    const int wave = tid >> 6, lane = tid & 63;
+    const int steps = (KC + 63) / 64;
+    // wave w of workgroup b takes row groups (b * NW + w) * RW, then every
+    // grid-stride after it: each workgroup builds x' once for all its rows
+    const int64_t stride = (int64_t)gridDim.x * NW * RW;
+    int64_t n0 = ((int64_t)blockIdx.x * NW + wave) * RW;
+    u32x4 wv[U][RW];
+    // Every load is issued, from a clamped (valid) address: without branches
+    // the compiler counts the loads in flight and waits only for the block it
+    // uses.  Chunks past K and rows past N are loaded and never used.
+    auto load_block = [&](int64_t nb, int s0) {
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int c = min(lane + 64 * (s0 + u), KC - 1);
+#pragma unroll
+            for (int r = 0; r < RW; ++r) {
+                const int64_t row = nb + r < p.N ? nb + r : p.N - 1;
+                wv[u][r] = *(const u32x4 *)(p.w + row * p.K + 8 * c);
+            }
+        }
+    };
+    // the first weights do not depend on x: in flight while the prologue runs
+    load_block(n0, 0);
+
+    if (PRO == kNorm) {
+        float ss = 0.f;
+        for (int c = tid; c < KC; c += GT) {
+            const u32x4 v = *(const u32x4 *)(p.x + 8 * c);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const float a = E::lo(v[i]), b = E::hi(v[i]);
+                ss = __builtin_fmaf(a, a, ss);
+                ss = __builtin_fmaf(b, b, ss);
+            }
+        }
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) ss += __shfl_xor(ss, o);
+        if (lane == 0) red[wave] = ss;
+        __syncthreads();
+        float tot = 0.f;
+#pragma unroll
+        for (int i = 0; i < NW; ++i) tot += red[i];
+        const float inv = 1.0f / sqrtf(tot / (float)p.K + p.eps);
+        for (int c = tid; c < KC; c += GT) {
+            const u32x4 v = *(const u32x4 *)(p.x + 8 * c);
+            const u32x4 g = *(const u32x4 *)(p.ln + 8 * c);
+            u32x4 o;
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                o[i] = E::pack2(E::lo(v[i]) * inv * E::lo(g[i]), E::hi(v[i]) * inv * E::hi(g[i]));
+            *(u32x4 *)(xs + 8 * c) = o;
+        }
+    } else if (PRO == kSilu) {
+        for (int c = tid; c < KC; c += GT) {
+            const u32x4 g = *(const u32x4 *)(p.x + 8 * c);
+            const u32x4 u = *(const u32x4 *)(p.x + p.K + 8 * c);
+            u32x4 o;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const float g0 = E::lo(g[i]), g1 = E::hi(g[i]);
+                o[i] = E::pack2(g0 / (1.0f + expf(-g0)) * E::lo(u[i]), g1 / (1.0f + expf(-g1)) * E::hi(u[i]));
+            }
+            *(u32x4 *)(xs + 8 * c) = o;
+        }
+    } else {
+        for (int c = tid; c < KC; c += GT) *(u32x4 *)(xs + 8 * c) = *(const u32x4 *)(p.x + 8 * c);
+    }
+    __syncthreads();
+
+    for (; n0 < p.N; n0 += stride) {
+        const int rows = p.N - n0 < RW ? (int)(p.N - n0) : RW;
+        float acc[RW];
+#pragma unroll
+        for (int r = 0; r < RW; ++r) acc[r] = 0.f;
+        for (int s0 = 0; s0 < steps; s0 += U) {
+            u32x4 cur[U][RW];
+#pragma unroll
+            for (int u = 0; u < U; ++u)
+#pragma unroll
+                for (int r = 0; r < RW; ++r) cur[u][r] = wv[u][r];
+            // the next block streams in meanwhile: of this row group, or the
+            // first of the next one
+            if (s0 + U < steps) load_block(n0, s0 + U);
+            else load_block(n0 + stride, 0);
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int c = lane + 64 * (s0 + u);
+                if (c < KC) {
+                    const u32x4 xv = *(const u32x4 *)(xs + 8 * c);
+#pragma unroll
+                    for (int r = 0; r < RW; ++r)
+#pragma unroll
+                        for (int i = 0; i < 4; ++i) {
+                            acc[r] = __builtin_fmaf(E::lo(cur[u][r][i]), E::lo(xv[i]), acc[r]);
+                            acc[r] = __builtin_fmaf(E::hi(cur[u][r][i]), E::hi(xv[i]), acc[r]);
+                        }
+                }
+            }
+        }
+#pragma unroll
+        for (int r = 0; r < RW; ++r)
+#pragma unroll
+            for (int o = 32; o > 0; o >>= 1) acc[r] += __shfl_xor(acc[r], o);
+        if (lane < rows) {
+            float v = acc[0];
+#pragma unroll
+            for (int r = 1; r < RW; ++r)
+                if (lane == r) v = acc[r];
+            if (p.beta) v += E::lo((uint32_t)p.y[n0 + lane]);
+            p.y[n0 + lane] = (uint16_t)(E::pack2(v, 0.f) & 0xffffu);
+        }
+    }
+}
+
 int grid_of(int64_t threads) {
     const int64_t b = (threads + NT - 1) / NT;
     return (int)(b < 16384 ? (b > 0 ? b : 1) : 16384);
@@ -175,11 +323,16 @@ struct Gemm {
     }
 };
 
+int gemv(int32_t dtype, int pro, const void *x, const void *ln, float eps, const void *w, int32_t K, int64_t N,
+         int beta, void *y, hipStream_t s);
+
 // y = x w^T (+ y): in column-major terms y^T [n_out x rows] = w^T [n_out x n_in]
 // (w stored as an n_in x n_out column-major matrix, transposed) times
 // x^T [n_in x rows].
 int linear(Blas *bl, int32_t dtype, const void *x, const void *w, int64_t rows, int32_t n_in, int32_t n_out,
            float beta, void *y, void *ws, size_t ws_bytes, hipStream_t s) {
+    if (rows == 1 && n_in <= kGemvMaxK)
+        return gemv(dtype, kPlain, x, nullptr, 0.f, w, n_in, n_out, beta != 0.f ? 1 : 0, y, s);
     const hipDataType ty = dtype == KVR_F16 ? HIP_R_16F : HIP_R_16BF;
     Gemm g;
     if (hipblasLtMatmulDescCreate(&g.op, HIPBLAS_COMPUTE_32F, HIP_R_32F) != HIPBLAS_STATUS_SUCCESS)
@@ -210,6 +363,34 @@ int linear(Blas *bl, int32_t dtype, const void *x, const void *w, int64_t rows, 
     const hipblasStatus_t st = hipblasLtMatmul(bl->h, g.op, &alpha, w, g.a, x, g.b, &beta, y, g.c, y, g.c,
                                                &it->second, ws, ws_bytes, s);
     return st == HIPBLAS_STATUS_SUCCESS ? KVR_OK : KVR_ERR_DEVICE;
+}
+
+// One-row product: at most kGemvMaxGrid workgroups of GT threads, one row per
+// wave and step (two for outputs of 65536 rows and more).
+int gemv(int32_t dtype, int pro, const void *x, const void *ln, float eps, const void *w, int32_t K, int64_t N,
+         int beta, void *y, hipStream_t s) {
+    GemvParams g;
+    g.x = (const uint16_t *)x;
+    g.w = (const uint16_t *)w;
+    g.ln = (const uint16_t *)ln;
+    g.y = (uint16_t *)y;
+    g.N = N;
+    g.K = K;
+    g.beta = beta;
+    g.eps = eps;
+    const int rw = N >= 65536 ? 2 : 1;
+    const int64_t groups = (N + rw * (GT / 64) - 1) / (rw * (GT / 64));
+    const dim3 grid((unsigned)(groups < kGemvMaxGrid ? groups : kGemvMaxGrid));
+#define KVR_GEMV(E_, P_, R_) hipLaunchKernelGGL((gemv_kernel<E_, P_, R_>), grid, dim3(GT), 0, s, g)
+#define KVR_GEMV_RW(E_, P_) do { if (rw == 2) KVR_GEMV(E_, P_, 2); else KVR_GEMV(E_, P_, 1); } while (0)
+#define KVR_GEMV_PRO(E_) do { if (pro == kNorm) KVR_GEMV_RW(E_, kNorm); else if (pro == kSilu) KVR_GEMV_RW(E_, kSilu); \
+                              else KVR_GEMV_RW(E_, kPlain); } while (0)
+    if (dtype == KVR_F16) KVR_GEMV_PRO(F16);
+    else KVR_GEMV_PRO(Bf16);
+#undef KVR_GEMV_PRO
+#undef KVR_GEMV_RW
+#undef KVR_GEMV
+    return hipGetLastError() == hipSuccess ? KVR_OK : KVR_ERR_DEVICE;
 }
 
 int check_shape(const kvr_desc *d, const kvr_layer_shape *sh) {
@@ -342,10 +523,19 @@ int kvr_layer_forward(const kvr_desc *desc, const kvr_layer_shape *shape, const 
     const int Wq = (Hq + 2 * Hkv) * D;
     void *blws = b + lw.blas;
 
+    // one token: the one-row products with the norms and the activation in
+    // their prologues; more tokens: separate norm / activation kernels and
+    // hipBLASLt products
+    const bool one = T == 1 && H <= kGemvMaxK && I <= kGemvMaxK && Hq * D <= kGemvMaxK;
+
     // attention block
-    if ((st = kvr_rmsnorm(dt, h, w->ln1, T, H, shape->eps, b + lw.xn, stream))) return st;
-    if ((st = linear(bl, dt, b + lw.xn, w->wqkv, T, H, Wq, 0.f, b + lw.qkv, blws, KVR_BLAS_WORKSPACE_BYTES, s)))
-        return st;
+    if (one) {
+        if ((st = gemv(dt, kNorm, h, w->ln1, shape->eps, w->wqkv, H, Wq, 0, b + lw.qkv, s))) return st;
+    } else {
+        if ((st = kvr_rmsnorm(dt, h, w->ln1, T, H, shape->eps, b + lw.xn, stream))) return st;
+        if ((st = linear(bl, dt, b + lw.xn, w->wqkv, T, H, Wq, 0.f, b + lw.qkv, blws, KVR_BLAS_WORKSPACE_BYTES, s)))
+            return st;
+    }
     QkParams qp;
     qp.qkv = (const uint16_t *)(b + lw.qkv);
     qp.qn = (const uint16_t *)w->q_norm;
@@ -382,6 +572,10 @@ int kvr_layer_forward(const kvr_desc *desc, const kvr_layer_shape *shape, const 
     if ((st = linear(bl, dt, b + lw.att, w->wo, T, Hq * D, H, 1.f, h, blws, KVR_BLAS_WORKSPACE_BYTES, s)))
         return st;
     // MLP block
+    if (one) {
+        if ((st = gemv(dt, kNorm, h, w->ln2, shape->eps, w->wgu, H, 2 * I, 0, b + lw.gu, s))) return st;
+        return gemv(dt, kSilu, b + lw.gu, nullptr, 0.f, w->wd, I, H, 1, h, s);
+    }
     if ((st = kvr_rmsnorm(dt, h, w->ln2, T, H, shape->eps, b + lw.xn, stream))) return st;
     if ((st = linear(bl, dt, b + lw.xn, w->wgu, T, H, 2 * I, 0.f, b + lw.gu, blws, KVR_BLAS_WORKSPACE_BYTES, s)))
         return st;

@@ -77,10 +77,22 @@ def test_rmsnorm_and_linear():
     M.kvr_linear(blas, y, wt, res, beta=1.0)                       # in place: y += x w^T
     want2 = ORope.round_to(np64(out) + acc, "bf16")
     assert np.all(np.abs(np64(res) - want2) <= 2.0 ** -7 * np.abs(want2) + 1e-6)
+    # one row: the streaming kernel (plain and accumulating), a wide and a narrow output
+    for n_out in (6144, 2560, 152):
+        w1 = wt[:n_out].contiguous()
+        o1 = torch.empty((1, n_out), dtype=BF, device=DEV)
+        M.kvr_linear(blas, y[5:6], w1, o1)
+        a1 = np64(y[5:6]) @ np64(w1).T
+        assert np.all(np.abs(np64(o1) - ORope.round_to(a1, "bf16")) <= 2.0 ** -7 * np.abs(a1) + 1e-6), n_out
+        r1 = o1.clone()
+        M.kvr_linear(blas, y[5:6], w1, r1, beta=1.0)
+        w2 = ORope.round_to(np64(o1) + a1, "bf16")
+        assert np.all(np.abs(np64(r1) - w2) <= 2.0 ** -7 * np.abs(w2) + 1e-6), n_out
     torch.cuda.synchronize()
 
 
-@pytest.mark.parametrize("cfg,Lp,S", [(SMALL, 70, 9), (SMALL, 200, 1), (QWEN, 40, 5)])
+# S = 1 takes the one-token path (norms and activation inside the one-row products)
+@pytest.mark.parametrize("cfg,Lp,S", [(SMALL, 70, 9), (SMALL, 200, 1), (QWEN, 40, 5), (QWEN, 40, 1)])
 def test_layer_vs_oracle(cfg, Lp, S):
     say("layer %d/%d Lp=%d S=%d" % (cfg["hidden"], cfg["intermediate"], Lp, S))
     n = Lp + S
@@ -129,7 +141,8 @@ def test_model_claim1_and_logits():
     full = m1.prefill(h.clone())
     lf = m1.logits(full).clone()
     part = m2.prefill(h[:Lp].clone())
-    rest = m2.step(h[Lp:].clone())
+    # the continuation: S - 3 tokens in one call, then three one-token steps
+    rest = torch.cat([m2.step(h[Lp:n - 3].clone())] + [m2.step(h[t:t + 1].clone()) for t in range(n - 3, n)])
     lr = m2.logits(rest).clone()
     torch.cuda.synchronize()
     dh = float((full[Lp:].double() - rest.double()).abs().max())
