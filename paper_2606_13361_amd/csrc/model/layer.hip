@@ -501,6 +501,8 @@ int kvr_layer_forward(const kvr_desc *desc, const kvr_layer_shape *shape, const 
     int st = check_shape(desc, shape);
     if (st) return st;
     if (T < 0 || T > ((int64_t)1 << 24) || L_prefix < 0) return KVR_ERR_SHAPE;
+    // one wave per (token, head) of the q/k/v rows: the grid must fit 32 bits
+    if (T * (desc->n_q_heads + 2 * (int64_t)desc->n_kv_heads) > 0x7fffffffLL) return KVR_ERR_SHAPE;
     if (L_prefix + T > desc->capacity) return KVR_ERR_CAPACITY;
     if (T == 0) return KVR_OK;
     if (!w || !rope || !blas || !h || !kcache || !vcache || !ws) return KVR_ERR_NULL;

@@ -63,6 +63,8 @@ def test_layer_forward_errors(mlib):
     assert fwd(mlib, sh=shape(reserved=1)) == kvr.KVR_ERR_SHAPE
     assert fwd(mlib, sh=shape(eps=-1.0)) == kvr.KVR_ERR_SHAPE
     assert fwd(mlib, T=-1) == kvr.KVR_ERR_SHAPE
+    # (token, head) waves beyond a 32-bit grid
+    assert fwd(mlib, d=desc(n_q_heads=4096, n_kv_heads=8, capacity=1 << 24), T=1 << 19) == kvr.KVR_ERR_SHAPE
     assert fwd(mlib, d=desc(capacity=100), T=50, Lp=60) == kvr.KVR_ERR_CAPACITY
     assert fwd(mlib, T=0, w="null", rope="null", blas=None, h=None) == kvr.KVR_OK
     assert fwd(mlib, w="null") == kvr.KVR_ERR_NULL
