@@ -111,7 +111,7 @@ def main():
     dout = torch.empty_like(dq)
     ws_dec = kvr.workspace_for(desc, n, 1)
 
-    names = ["prefill", "continue", "append", "readers", "decode_continue", "decode_append"]
+    names = ["prefill", "continue", "append", "readers", "decode_step"]
 
     def step(ev=None):
         def rec(i):
@@ -126,10 +126,8 @@ def main():
         rec(3)
         kvr.kvr_continue_batched(desc, rq, rk, rv, cu, kc, vc, L, rout)
         rec(4)
-        kvr.kvr_continue(desc, dq, dk, dv, kc, vc, n, 1, dout, ws_dec)
+        kvr.kvr_continue_append(desc, dq, dk, dv, kc, vc, n, 1, dout, ws_dec)
         rec(5)
-        kvr.kvr_cache_append(desc, dk, dv, 1, kc, vc, n)
-        rec(6)
 
     if args.model_only:
         print(json.dumps({"model": model_table1(torch, A, W, dev)}), flush=True)
@@ -145,7 +143,7 @@ def main():
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    events = [[torch.cuda.Event(enable_timing=True) for _ in range(7)] for _ in range(args.steps)]
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(len(names) + 1)] for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
@@ -165,7 +163,7 @@ def main():
     c_gbps = c_bytes / avg["continue"] / 1e9
     rd_flops = A.batched_flops(L, lens, Hq, D)
     rd_tflops = rd_flops / avg["readers"] / 1e12
-    dec_bytes = A.continue_bytes(n, 1, Hq, Hkv, D, ELT)
+    dec_bytes = A.continue_bytes(n, 1, Hq, Hkv, D, ELT) + A.append_bytes(1, Hkv, D, ELT)
 
     # parity spot check of this very run (continuation vs prefill rows, Claim 1)
     claim1 = float((out_c - out_full[L:]).abs().max())
@@ -204,8 +202,8 @@ def main():
         "readers_ms": round(avg["readers"] * 1e3, 4),
         "readers_tflops": round(rd_tflops, 2),
         "readers_mfma_frac": round(rd_tflops / PEAK_BF16_TFLOPS, 4),
-        "decode_step_us": round((avg["decode_continue"] + avg["decode_append"]) * 1e6, 2),
-        "decode_continue_GBps": round(dec_bytes / avg["decode_continue"] / 1e9, 1),
+        "decode_step_us": round(avg["decode_step"] * 1e6, 2),
+        "decode_step_GBps": round(dec_bytes / avg["decode_step"] / 1e9, 1),
         "median_ms": {nm: round(med[nm] * 1e3, 4) for nm in names},
         "claim1_maxabs": claim1,
         "paper_context": "paper Table 1: full-model reuse 8.6-49.7x cheaper (Qwen3-4B fp16, Apple M1 Pro "
@@ -421,7 +419,7 @@ def sweep(torch, kvr, A, W, dev, stream, lengths, suffix=None):
 
 
 def decode36(torch, kvr, A, W, dev, stream):
-    """36 layers x 24 decode steps: continue(S=1) over 32768+t cached rows, then append."""
+    """36 layers x 24 decode steps: continue(S=1) over 32768+t cached rows and the cache update."""
     sh = W.QWEN
     Hq, Hkv, D = sh.n_q_heads, sh.n_kv_heads, sh.head_dim
     Lz, T, NL = W.DECODE_L, W.DECODE_STEPS, W.DECODE_LAYERS
@@ -436,34 +434,47 @@ def decode36(torch, kvr, A, W, dev, stream):
     out = torch.empty((1, Hq, D), dtype=torch.bfloat16, device=dev)
     ws = kvr.workspace_for(desc, cap, 1)
 
-    def run_chain():
-        for t in range(T):
-            for l in range(NL):
-                x = qkv[t, l]
-                qq = x[:Hq].unsqueeze(0)
-                kk = x[Hq:Hq + Hkv].unsqueeze(0)
-                vv = x[Hq + Hkv:].unsqueeze(0)
-                kvr.kvr_continue(desc, qq, kk, vv, caches[l, 0], caches[l, 1], Lz + t, 1, out, ws)
-                kvr.kvr_cache_append(desc, kk, vv, 1, caches[l, 0], caches[l, 1], Lz + t)
+    def chain(fused):
+        def run():
+            for t in range(T):
+                for l in range(NL):
+                    x = qkv[t, l]
+                    qq = x[:Hq].unsqueeze(0)
+                    kk = x[Hq:Hq + Hkv].unsqueeze(0)
+                    vv = x[Hq + Hkv:].unsqueeze(0)
+                    if fused:     # attention and the cache update in one call
+                        kvr.kvr_continue_append(desc, qq, kk, vv, caches[l, 0], caches[l, 1], Lz + t, 1, out, ws)
+                    else:
+                        kvr.kvr_continue(desc, qq, kk, vv, caches[l, 0], caches[l, 1], Lz + t, 1, out, ws)
+                        kvr.kvr_cache_append(desc, kk, vv, 1, caches[l, 0], caches[l, 1], Lz + t)
+        return run
 
+    run_chain = chain(True)
     run_chain()
     torch.cuda.synchronize()
     ts = timed(torch, stream, lambda i: run_chain(), 3)
     t_eager = sum(ts) / len(ts)
-    # the whole chain (864 continue + 864 append calls) as one HIP graph
-    t_avg = graph_time(torch, stream, run_chain, 1, replays=3)
+    # the whole chain (864 calls) as one HIP graph; then the same work as
+    # separate continue and append calls
+    t_graph = graph_time(torch, stream, run_chain, 1, replays=3)
+    t_sep = graph_time(torch, stream, chain(False), 1, replays=3)
+    t_avg = min(t_graph, t_eager)
     by = sum(A.continue_bytes(Lz + t, 1, Hq, Hkv, D, 2) + A.append_bytes(1, Hkv, D, 2)
              for t in range(T)) * NL
     res = {
         "layers": NL, "prefix": Lz, "steps": T,
         "chain_ms": round(t_avg * 1e3, 3),
+        "chain_graph_ms": round(t_graph * 1e3, 3),
         "chain_eager_ms": round(t_eager * 1e3, 3),
+        "chain_separate_update_ms": round(t_sep * 1e3, 3),
         "per_call_us": round(t_avg / (T * NL) * 1e6, 2),
         "GBps": round(by / t_avg / 1e9, 1),
         "hbm_frac": round(by / t_avg / 1e9 / PEAK_HBM_GBPS, 4),
         "resident_cache_GB": round(caches.numel() * 2 / 1e9, 3),
-        "note": "continue + append per layer per step; timed as one HIP-graph replay of the chain "
-                "(chain_eager_ms: host-issued launches)",
+        "note": "kvr_continue_append per layer per step (the attention and its cache update in one call); "
+                "chain_ms is the faster of one HIP-graph replay of the chain (chain_graph_ms) and host-issued "
+                "launches (chain_eager_ms); chain_separate_update_ms: kvr_continue then kvr_cache_append, "
+                "graph-replayed",
     }
     del caches, qkv
     torch.cuda.empty_cache()

@@ -130,6 +130,21 @@ int kvr_continue_batched(const kvr_desc *desc, const void *Qs, const void *Ks, c
                          size_t ws_bytes, void *stream);
 
 /*
+ * kvr_continue followed by the cache update of its tokens (Alg. 2's forward
+ * call and cache update; a decode step when S == 1): out as kvr_continue
+ * computes it over cache rows [0, L_prefix), and cache rows
+ * [L_prefix, L_prefix + S) receive Ks/Vs unchanged, exactly as
+ * kvr_cache_append(desc, Ks, Vs, S, kcache, vcache, L_prefix) writes them.
+ * Needs L_prefix + S <= capacity.  For 16-bit continuations at head_dim 128
+ * with (n_q_heads / n_kv_heads) * S <= 96 the attention kernel stores the
+ * rows itself (one launch fewer); other shapes issue the update after it.
+ * ws as for kvr_continue.
+ */
+int kvr_continue_append(const kvr_desc *desc, const void *Qs, const void *Ks, const void *Vs,
+                        void *kcache, void *vcache, int64_t L_prefix, int64_t S, void *out,
+                        void *ws, size_t ws_bytes, void *stream);
+
+/*
  * Cache write: rows [L_cur, L_cur+S) of each kv head receive Ks/Vs
  * [S][Hkv][d] unchanged (Alg. 2's cache update after a decode step).
  * Needs 0 <= L_cur and L_cur + S <= capacity.  Other rows are untouched.

@@ -81,6 +81,26 @@ struct F16 {
     __device__ static __forceinline__ float hi(uint32_t w) { return (float)__builtin_bit_cast(f16x2, w)[1]; }
 };
 
+// The cache update of a continuation, done by one workgroup per kv head after
+// its attention work: the S new K and V rows of kv head g (token-major inputs)
+// into cache rows [n_prefix, n_prefix + S), 16-byte chunks spread over the
+// calling threads.  The attention reads cache rows [0, n_prefix) only, so the
+// stores never meet a read of the same launch.
+template <int ROWB>
+__device__ __forceinline__ void append_new_rows(const AttnParams &p, int g, int S, int tid, int nthreads) {
+    constexpr int CH = ROWB / 16;
+    const int64_t nstride = (int64_t)p.n_kv_heads * ROWB;
+    for (int i = tid; i < 2 * S * CH; i += nthreads) {
+        const int half = i / (S * CH);                 // 0: K, 1: V
+        const int rem = i - half * S * CH;
+        const int t = rem / CH, c = rem - t * CH;
+        const unsigned char *src = (const unsigned char *)(half ? p.vn : p.kn) + t * nstride + g * ROWB + 16 * c;
+        unsigned char *dst = (unsigned char *)(half ? p.vc_app : p.kc_app) +
+                             ((int64_t)g * p.cap + p.n_prefix + t) * ROWB + 16 * c;
+        *(u32x4 *)dst = *(const u32x4 *)src;
+    }
+}
+
 // Rotary position embedding of one pair (x1, x2) = (x[i], x[i + d/2]) by the
 // angle whose cosine and sine are c and s (rotary embedding of Su et al. in
 // the half-split pairing).  Written with explicit fused multiply-adds so that

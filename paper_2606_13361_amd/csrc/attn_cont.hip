@@ -503,6 +503,7 @@ __global__ __launch_bounds__(THREADS) void attn_cont_kernel(const AttnParams p) 
         case 2: finish_quarter<E, NCT, 2>(p, rs, obuf, lbuf, mbuf, valid, tok, head, g, split, lane); break;
         default: finish_quarter<E, NCT, 3>(p, rs, obuf, lbuf, mbuf, valid, tok, head, g, split, lane); break;
     }
+    if (!Q8 && p.kc_app && (p.nsplit == 1 || last_split)) append_new_rows<ROWB>(p, g, S, tid, THREADS);
 }
 
 }  // namespace

@@ -305,7 +305,11 @@ __global__ __launch_bounds__(RTHREADS) void attn_rows_kernel(const AttnParams p)
     }
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");
-    if (par == 1) return;
+    if (par == 1) {
+        // the waves of parity 1 are done: they store the cache update, if any
+        if (p.kc_app && split == p.nsplit - 1) append_new_rows<ROWB>(p, g, S, tid - 256, 256);
+        return;
+    }
     {
         const float m1 = xml[lane], l1 = xml[64 + lane];
         const float M = fmaxf(rs.m, m1);

@@ -164,7 +164,8 @@ int append_impl(const kvr_desc *d, const void *Ks, const void *Vs, int64_t S, vo
 // RoPE pre-pass wrote them there); the kernel then writes no cache rows.
 int launch_single(const kvr_desc *d, int mode, const void *Q, const void *K, const void *V, void *kc,
                   void *vc, int64_t n_prefix, int64_t n_tok, void *out, const Split &sp, void *ws,
-                  hipStream_t stream, const float *qscale = nullptr, const float *rope = nullptr) {
+                  hipStream_t stream, const float *qscale = nullptr, const float *rope = nullptr,
+                  bool append = false) {
     AttnParams p;
     fill_common(p, d);
     p.q = Q; p.kn = K; p.vn = V; p.out = out;
@@ -214,6 +215,11 @@ int launch_single(const kvr_desc *d, int mode, const void *Q, const void *K, con
         // artifact use the kernel whose waves split the keys.
         const int nct = (int)((rows + 31) / 32);
         const int64_t keys_per_wg = p.nsplit > 1 ? p.chunk : n_prefix + n_tok;
+        if (append) {            // both kernels store the new rows themselves
+            p.kc_app = kc;
+            p.vc_app = vc;
+            append = false;
+        }
         if (qscale || nct == 1 || keys_per_wg > kRowsSplitMaxKeys)
             e = launch_attn_cont(p, nct, qscale != nullptr, f16(d), (int)grid, stream);
         else
@@ -232,6 +238,10 @@ int launch_single(const kvr_desc *d, int mode, const void *Q, const void *K, con
         e = launch_attn_f32(p, d->head_dim, (int)grid, stream);
     }
     if (e != hipSuccess) return KVR_ERR_DEVICE;
+    if (append) {                // the other kernels: the cache update as its own launch
+        const int st = append_impl(d, K, V, n_tok, kc, vc, n_prefix, stream);
+        if (st) return st;
+    }
     if (p.nsplit > 1) {
         MergeParams m;
         m.ws = p.ws; m.out = out; m.nsplit = p.nsplit; m.n_q_heads = p.n_q_heads;
@@ -379,6 +389,25 @@ int kvr_continue(const kvr_desc *desc, const void *Qs, const void *Ks, const voi
         return KVR_ERR_ALIGN;
     return launch_single(desc, kModeContinue, Qs, Ks, Vs, (void *)kcache, (void *)vcache, L_prefix, S, out,
                          sp, ws, (hipStream_t)stream);
+}
+
+int kvr_continue_append(const kvr_desc *desc, const void *Qs, const void *Ks, const void *Vs, void *kcache,
+                        void *vcache, int64_t L_prefix, int64_t S, void *out, void *ws, size_t ws_bytes,
+                        void *stream) {
+    int st = check_desc(desc);
+    if (st) return st;
+    if (L_prefix < 0 || S < 0 || S > kMaxTokens || L_prefix > kMaxKeys) return KVR_ERR_SHAPE;
+    if (L_prefix + S > desc->capacity) return KVR_ERR_CAPACITY;
+    if (S == 0) return KVR_OK;
+    if (!Qs || !Ks || !Vs || !out || !kcache || !vcache) return KVR_ERR_NULL;
+    const Split sp = plan_split(desc, L_prefix, S);
+    if (ws_bytes < sp.ws_bytes) return KVR_ERR_WORKSPACE;
+    if (sp.ws_bytes > 0 && !ws) return KVR_ERR_NULL;
+    if (!aligned16(Qs) || !aligned16(Ks) || !aligned16(Vs) || !aligned16(out) || !aligned16(kcache) ||
+        !aligned16(vcache) || !aligned16(ws))
+        return KVR_ERR_ALIGN;
+    return launch_single(desc, kModeContinue, Qs, Ks, Vs, kcache, vcache, L_prefix, S, out, sp, ws,
+                         (hipStream_t)stream, nullptr, nullptr, true);
 }
 
 size_t kvr_q8_bytes(const kvr_desc *desc) {

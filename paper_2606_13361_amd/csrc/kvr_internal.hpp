@@ -34,6 +34,11 @@ struct AttnParams {
     // (n_kv_heads * D, D); prefill with RoPE reads its rotated rows back from
     // the cache, (D, cap * D).  Honoured by the prefill / readers kernels.
     int64_t new_tok_stride, new_head_stride;
+    // Continuation with the cache update: the workgroup that reads the new
+    // rows of a kv head last (the last split) also stores them into rows
+    // [n_prefix, n_prefix + S) of these caches; null: no update.  Honoured by
+    // the keys-split and row-split continuation kernels.
+    void *kc_app, *vc_app;
     int64_t cap;
     int64_t n_prefix;  // cached keys, positions [0, n_prefix); every query row sees them all
     int64_t chunk;     // prefix keys per split, a multiple of the key tile

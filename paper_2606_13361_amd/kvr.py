@@ -21,7 +21,7 @@ KVR_ERR_MISMATCH, KVR_ERR_POSITION = 8, 9
 KVR_ARTIFACT_HEADER_BYTES = 256
 KVR_BF16, KVR_F32, KVR_F16 = 0, 1, 2
 
-EXPORTS = ("kvr_prefill", "kvr_continue", "kvr_continue_batched", "kvr_cache_append",
+EXPORTS = ("kvr_prefill", "kvr_continue", "kvr_continue_append", "kvr_continue_batched", "kvr_cache_append",
            "kvr_workspace_bytes", "kvr_strerror", "kvr_abi_version",
            "kvr_q8_bytes", "kvr_quantize_cache", "kvr_continue_q8",
            "kvr_artifact_bytes", "kvr_artifact_save", "kvr_artifact_load",
@@ -64,6 +64,7 @@ def load():
     D = ctypes.POINTER(kvr_desc)
     lib.kvr_prefill.argtypes = [D, P, P, P, I64, P, P, P, P]
     lib.kvr_continue.argtypes = [D, P, P, P, P, P, I64, I64, P, P, SZ, P]
+    lib.kvr_continue_append.argtypes = [D, P, P, P, P, P, I64, I64, P, P, SZ, P]
     lib.kvr_continue_batched.argtypes = [D, P, P, P, ctypes.POINTER(ctypes.c_int32), ctypes.c_int32,
                                          P, P, I64, P, P, SZ, P]
     lib.kvr_cache_append.argtypes = [D, P, P, I64, P, P, I64, P]
@@ -91,7 +92,8 @@ def load():
     lib.kvr_strerror.argtypes = [ctypes.c_int]
     lib.kvr_strerror.restype = ctypes.c_char_p
     lib.kvr_abi_version.argtypes = []
-    for f in (lib.kvr_prefill, lib.kvr_continue, lib.kvr_continue_batched, lib.kvr_cache_append,
+    for f in (lib.kvr_prefill, lib.kvr_continue, lib.kvr_continue_append, lib.kvr_continue_batched,
+              lib.kvr_cache_append,
               lib.kvr_abi_version, lib.kvr_quantize_cache, lib.kvr_continue_q8, lib.kvr_artifact_save,
               lib.kvr_artifact_load, lib.kvr_rope_table, lib.kvr_rope_apply, lib.kvr_prefill_rope,
               lib.kvr_continue_rope, lib.kvr_continue_batched_rope):
@@ -176,6 +178,19 @@ def kvr_continue(desc, Qs, Ks, Vs, kcache, vcache, L_prefix, S, out, ws=None, st
     wp, wn = _workspace(ws)
     _raise(load().kvr_continue(ctypes.byref(desc), q, k, v, kc, vc, int(L_prefix), int(S), o, wp, wn,
                                _stream(stream)), "kvr_continue")
+
+
+def kvr_continue_append(desc, Qs, Ks, Vs, kcache, vcache, L_prefix, S, out, ws=None, stream=None):
+    """kvr_continue plus the cache update of the S tokens at rows L_prefix.. ."""
+    Hq, Hkv, d = desc.n_q_heads, desc.n_kv_heads, desc.head_dim
+    q = _check(Qs, "Qs", desc, (S, Hq, d))
+    k = _check(Ks, "Ks", desc, (S, Hkv, d))
+    v = _check(Vs, "Vs", desc, (S, Hkv, d))
+    o = _check(out, "out", desc, (S, Hq, d))
+    kc, vc = _cache_ptrs(desc, kcache, vcache, True)
+    wp, wn = _workspace(ws)
+    _raise(load().kvr_continue_append(ctypes.byref(desc), q, k, v, kc, vc, int(L_prefix), int(S), o, wp, wn,
+                                      _stream(stream)), "kvr_continue_append")
 
 
 def kvr_continue_batched(desc, Qs, Ks, Vs, cu_seqlens, kcache, vcache, L_prefix, out, ws=None,

@@ -261,3 +261,15 @@ def test_continue_q8_errors(lib):
     d2 = desc(capacity=8192)
     need = lib.kvr_workspace_bytes(ctypes.byref(d2), 4096, 24, 1)
     assert cont_q8(lib, d2, Lp=4096, S=24, wsb=need - 1) == kvr.KVR_ERR_WORKSPACE
+
+
+def test_continue_append_errors(lib):
+    d = desc(capacity=100)
+    f = lambda Lp=64, S=8, Q=A, K=A, V=A, kc=A, vc=A, out=A, ws=A, wsb=1 << 30: lib.kvr_continue_append(  # noqa: E731
+        ctypes.byref(d), Q, K, V, kc, vc, Lp, S, out, ws, wsb, None)
+    assert f(Lp=-1) == kvr.KVR_ERR_SHAPE
+    assert f(Lp=95, S=8) == kvr.KVR_ERR_CAPACITY          # the update needs rows 95..102
+    assert f(S=0, Q=None, K=None, V=None, kc=None, vc=None, out=None) == kvr.KVR_OK
+    for kw in ("Q", "K", "V", "out", "kc", "vc"):
+        assert f(**{kw: None}) == kvr.KVR_ERR_NULL, kw    # the caches are written: always needed
+        assert f(**{kw: MIS}) == kvr.KVR_ERR_ALIGN, kw
