@@ -38,6 +38,15 @@ __global__ __launch_bounds__(MERGE_THREADS) void merge_bf16_kernel(const MergePa
     const int64_t per_split = (int64_t)p.n_kv_heads * p.rows;
     const float *ml = p.ws + (int64_t)p.nsplit * per_split * D;
     const int64_t row = (int64_t)g * p.rows + (valid ? r : r0);   // rows past the end read row r0
+    const float *src = p.ws + row * D + 4 * part;
+    const int64_t sstride = per_split * D;
+
+    // the first MERGE_BATCH splits' partial rows do not depend on the
+    // weights: their loads go out before the (m, l) round trip (split indices
+    // past nsplit re-read the last split and are never used)
+    float4 o0[MERGE_BATCH];
+#pragma unroll
+    for (int k = 0; k < MERGE_BATCH; ++k) o0[k] = *(const float4 *)(src + min(k, p.nsplit - 1) * sstride);
 
     float M = -INFINITY;
     for (int s = part; s < p.nsplit; s += CPR) M = fmaxf(M, ml[(s * per_split + row) * 2]);
@@ -55,10 +64,19 @@ __global__ __launch_bounds__(MERGE_THREADS) void merge_bf16_kernel(const MergePa
     __syncthreads();
     if (!valid) return;
 
-    const float *src = p.ws + row * D + 4 * part;
-    const int64_t sstride = per_split * D;
     float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-    int s = 0;
+    const int n0 = p.nsplit < MERGE_BATCH ? p.nsplit : MERGE_BATCH;
+#pragma unroll
+    for (int k = 0; k < MERGE_BATCH; ++k) {
+        if (k < n0) {
+            const float w = wts[rr][k];
+            acc.x = __builtin_fmaf(w, o0[k].x, acc.x);
+            acc.y = __builtin_fmaf(w, o0[k].y, acc.y);
+            acc.z = __builtin_fmaf(w, o0[k].z, acc.z);
+            acc.w = __builtin_fmaf(w, o0[k].w, acc.w);
+        }
+    }
+    int s = n0;
     for (; s + MERGE_BATCH <= p.nsplit; s += MERGE_BATCH) {
         float4 o[MERGE_BATCH];
 #pragma unroll
