@@ -1,8 +1,10 @@
 // attn_bf16.hip -- causal grouped-query attention with a query offset, bf16
 // in, fp32 accumulate, for gfx950 (MI355X): the register-staged member of the
-// kernel family.  It serves prefill (all head dims) and every mode at head_dim
-// 64; continue and many-readers at head_dim 128 use the streamed kernel in
-// attn_stream.hip.  The per-tile arithmetic is shared (attn_common.hpp).
+// kernel family.  It serves every mode at head_dim 64 and continuations of
+// more than 96 query rows per kv head at head_dim 128; prefill and many
+// readers at head_dim 128 run on the two-group kernel (attn_pp.hip), shorter
+// continuations on attn_rows.hip / attn_cont.hip.  The per-tile arithmetic is
+// shared (attn_common.hpp).
 //
 //   prefill   keys are the new rows only, row tiles visited longest first, and
 //             the workgroup owning a token also writes its K/V row into the

@@ -1,7 +1,7 @@
-// attn_common.hpp -- device pieces shared by the two bf16 attention kernels
-// (register-staged tiles in attn_bf16.hip, direct-to-LDS streamed tiles in
-// attn_stream.hip): work-item decoding, the per-tile MFMA / online-softmax
-// step and the epilogue.
+// attn_common.hpp -- device pieces shared by the 16-bit attention kernels
+// (attn_bf16.hip, attn_pp.hip, attn_rows.hip, attn_cont.hip, merge.hip):
+// element formats, work-item decoding, the per-tile MFMA / online-softmax
+// step, the direct-to-LDS loads and the epilogue.
 //
 // Notation of one 64-key tile and one wave (32 query rows = MFMA columns):
 //   S^T[key][row] = K Q^T              v_mfma_f32_32x32x16_bf16, K from LDS,

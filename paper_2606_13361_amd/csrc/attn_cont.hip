@@ -18,7 +18,7 @@
 // stores that quarter of the workgroup's split partial -- or of the output
 // when there is no split.
 //
-// LDS tile layout as in the streamed kernel: 256-byte rows, 16-byte chunk c of
+// LDS tile layout as in the two-group kernel: 256-byte rows, 16-byte chunk c of
 // row r in slot c ^ swz(r), conflict-free for the K reads and the
 // transposing V reads.
 #include <type_traits>
@@ -272,7 +272,7 @@ __global__ __launch_bounds__(THREADS) void attn_cont_kernel(const AttnParams p) 
         }
     };
 
-    // ---- read maps (per lane, loop invariant); see the streamed kernel
+    // ---- read maps (per lane, loop invariant): K fragments and transposing V reads of the swizzled rows
     uint32_t ka[D / 16];
 #pragma unroll
     for (int ks = 0; ks < D / 16; ++ks) ka[ks] = (uint32_t)j * ROWB + 16u * (uint32_t)((2 * ks + grp) ^ swz(j));

@@ -175,7 +175,7 @@ __global__ __launch_bounds__(PP_THREADS) void attn_pp_kernel(const AttnParams p)
         for (int q = 0; q < PP_LOADS; ++q) dma_fast(f, q);
     };
 
-    // ---- read maps (per lane, loop invariant); as in the streamed kernel
+    // ---- read maps (per lane, loop invariant): K fragments and transposing V reads of the swizzled rows
     uint32_t ka[D / 16];
 #pragma unroll
     for (int ks = 0; ks < D / 16; ++ks) ka[ks] = (uint32_t)j * ROWB + 16u * (uint32_t)((2 * ks + grp) ^ swz(j));
