@@ -420,29 +420,39 @@ __global__ __launch_bounds__(PP_THREADS) void attn_pp_kernel(const AttnParams p)
         if (act) { __builtin_amdgcn_s_setprio(1); gemm_pv(ntiles); __builtin_amdgcn_s_setprio(0); }
     }
 
-    // ---- epilogue.  After this barrier no wave reads the ring any more; the
-    // last NS tiles are still in it.
-    __syncthreads();
-
-    if constexpr (MODE == kModePrefill) if (p.kc_out) {
-    // cache rows of the tokens whose first query row is in this workgroup, copied
-    // from the ring: those tokens are the workgroup's last keys (at most 256/G + 1
-    // of them, aligned so that they lie within the last four tiles)
-    const int own_lo = (row0 + G - 1) / G;
-    const int own_hi = row_last / G;               // inclusive, = ke - 1
-    const int n_own = own_hi >= own_lo ? own_hi - own_lo + 1 : 0;
-    unsigned char *kc = (unsigned char *)p.kc_out + ((int64_t)g * p.cap) * ROWB;
-    unsigned char *vc = (unsigned char *)p.vc_out + ((int64_t)g * p.cap) * ROWB;
-    for (int idx = tid; idx < n_own * 32; idx += PP_THREADS) {
-        const int tk = own_lo + (idx >> 5);
-        const int half = (idx >> 4) & 1;             // 0: K row, 1: V row
-        const int c = idx & 15;
-        const int r = tk & (KEYS - 1);
-        const unsigned char *src = smem + ((tk / KEYS) % NS) * STAGE + half * TILE + r * ROWB + 16 * (c ^ swz(r));
-        *(u32x4 *)((half ? vc : kc) + (int64_t)tk * ROWB + 16 * c) = *(const u32x4 *)src;
+    // ---- epilogue.  Every tile has landed and the ring is only read from here
+    // on.  Prefill: group A, idle while group B runs its last PV product, copies
+    // the cache rows of the tokens whose first query row is in this workgroup out
+    // of the ring: those tokens are the workgroup's last keys (at most 256/G + 1
+    // of them, aligned so that they lie within the last four tiles).  Four LDS
+    // reads go out before their four stores.
+    if constexpr (MODE == kModePrefill) if (p.kc_out && gw == 0) {
+        const int own_lo = (row0 + G - 1) / G;
+        const int own_hi = row_last / G;               // inclusive, = ke - 1
+        const int n_copy = own_hi >= own_lo ? (own_hi - own_lo + 1) * 32 : 0;
+        unsigned char *kc = (unsigned char *)p.kc_out + ((int64_t)g * p.cap) * ROWB;
+        unsigned char *vc = (unsigned char *)p.vc_out + ((int64_t)g * p.cap) * ROWB;
+        constexpr int A_THREADS = PP_THREADS / 2;
+        for (int base = tid; base < n_copy; base += 4 * A_THREADS) {
+            u32x4 v[4];
+            u32x4 *dp[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int idx = min(base + u * A_THREADS, n_copy - 1);   // past the end: re-read, not stored
+                const int tk = own_lo + (idx >> 5);
+                const int half = (idx >> 4) & 1;             // 0: K row, 1: V row
+                const int c = idx & 15;
+                const int r = tk & (KEYS - 1);
+                v[u] = *(const u32x4 *)(smem + ((tk / KEYS) % NS) * STAGE + half * TILE + r * ROWB + 16 * (c ^ swz(r)));
+                dp[u] = (u32x4 *)((half ? vc : kc) + (int64_t)tk * ROWB + 16 * c);
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+                if (base + u * A_THREADS < n_copy) *dp[u] = v[u];
+        }
     }
+    // after this barrier no wave reads the ring any more
     __syncthreads();
-    }
 
     // output rows through LDS: the wave's 32 rows in bf16 (pitch OPITCH), then 16
     // bytes per lane, 4 rows (one token's 4 heads for G = 4: 1 KB) per store
@@ -461,14 +471,16 @@ __global__ __launch_bounds__(PP_THREADS) void attn_pp_kernel(const AttnParams p)
                 *(u32x2 *)(ob + j * OPITCH + 2 * (32 * mt + 8 * q4 + 4 * grp)) = v;
             }
         asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // this wave's rows are in LDS
+        // all eight LDS reads before the stores
+        u32x4 v[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) v[i] = *(const u32x4 *)(ob + (4 * i + (lane >> 4)) * OPITCH + 16 * (lane & 15));
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
-            const int rr = 4 * i + (lane >> 4);
-            const int rw = wrow0 + rr;
+            const int rw = wrow0 + 4 * i + (lane >> 4);
             if (rw < R) {
-                const u32x4 v = *(const u32x4 *)(ob + rr * OPITCH + 16 * (lane & 15));
                 uint16_t *orow = (uint16_t *)p.out + ((int64_t)(tok0 + rw / G) * p.n_q_heads + g * G + rw % G) * D;
-                *(u32x4 *)(orow + 8 * (lane & 15)) = v;
+                *(u32x4 *)(orow + 8 * (lane & 15)) = v[i];
             }
         }
     }
