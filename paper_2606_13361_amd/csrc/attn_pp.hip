@@ -92,7 +92,15 @@ __global__ __launch_bounds__(PP_THREADS) void attn_pp_kernel(const AttnParams p)
     const bool wave_active = wrow0 < R;
     const int k_full = wave_active ? npre + wrow0 / G + 1 : 0;   // keys every row of this wave sees
 
-    u32x4 qf[D / 16];     // this lane's query row as MFMA operands, read from LDS before the loops
+    u32x4 qf[D / 16];
+    {
+        const uint16_t *qrow = (const uint16_t *)p.q + ((int64_t)(tok0 + tok) * p.n_q_heads + head) * D;
+#pragma unroll
+        for (int ks = 0; ks < D / 16; ++ks)
+            qf[ks] = valid ? *(const u32x4 *)(qrow + 16 * ks + 8 * grp) : (u32x4){0, 0, 0, 0};
+        // RoPE: the row is rotated once, at its own position
+        if (p.rope && valid) rope_q_frag<E, D>(qf, p.rope + (int64_t)pos * D, grp);
+    }
 
     // ---- load map: wave w moves K rows 8w..8w+7 and V rows 8w..8w+7 of a tile,
     // 4 rows per instruction; lane -> row 8w + 4i + lane/16, LDS slot lane%16,
@@ -351,42 +359,13 @@ __global__ __launch_bounds__(PP_THREADS) void attn_pp_kernel(const AttnParams p)
         }
         __builtin_amdgcn_sched_barrier(0);
     };
-    // The workgroup's query rows reach LDS first, in ring stages 2 and 3 (free
-    // until tile 2 is issued, after the first barrier): 1 KB contiguous per
-    // instruction (4 rows of 256 bytes: one token's G heads for G = 4), the same
-    // swizzle as the K/V tiles.  Wave w moves workgroup rows 32w .. 32w + 31;
-    // rows past R repeat row R - 1 (computed, never stored).  Then tiles 0 and 1.
-    {
-        const unsigned char *q_a = (const unsigned char *)p.q;
-        unsigned char *q_lds = smem + 2 * STAGE;
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            const int lr = 32 * wave + 4 * i + (lane >> 4);
-            const int rr = min(row0 + lr, R - 1);
-            const int64_t src_row = (int64_t)(tok0 + rr / G) * p.n_q_heads + g * G + rr % G;
-            dma16(q_a + src_row * ROWB + 16 * ((lane & 15) ^ swz(lr)), q_lds + (32 * wave + 4 * i) * ROWB);
-        }
-    }
     load_tile(0);
     if (ntiles > 1) load_tile(1);
-    // Q has landed once at most the loads of tiles 0 and 1 are in flight (the
-    // bound also holds if loads issued with no lane enabled were counted); the
-    // barrier makes every wave's rows visible.  Each wave reads its rows' MFMA
-    // operands (rows 32 * slot + j: the swizzle depends on j alone), rotates them
-    // for RoPE, and finishes these LDS reads before the first step's barrier,
-    // after which tile 2 may overwrite stage 2.
-    if (ntiles > 1) wait_vmcnt<2 * PP_LOADS>();
-    else wait_vmcnt<PP_LOADS>();
-    __builtin_amdgcn_s_barrier();
-    asm volatile("" ::: "memory");
-    {
-        const unsigned char *q_rows = smem + 2 * STAGE + 32 * (2 * (wave & 3) + gw) * ROWB;
-#pragma unroll
-        for (int ks = 0; ks < D / 16; ++ks) qf[ks] = *(const u32x4 *)(q_rows + ka[ks]);
-        // RoPE: the row is rotated once, at its own position
-        if (p.rope && valid) rope_q_frag<E, D>(qf, p.rope + (int64_t)pos * D, grp);
-    }
-    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    // One use of the Q fragments here, on every path: the compiler puts its wait
+    // for their loads (which also covers tiles 0 and 1, issued after them) at
+    // this point, and none in the loops below -- otherwise a path that reaches
+    // a loop without having used them makes it wait for every load in flight at
+    // the first product of each step.
 #pragma unroll
     for (int ks = 0; ks < D / 16; ++ks) asm volatile("" ::"v"(qf[ks]));
     const bool act = wave_active;
