@@ -201,7 +201,15 @@ __global__ __launch_bounds__(THREADS) void attn_cont_kernel(const AttnParams p) 
     const int n_cst = Q8 ? (ce > kb ? (int)((ce - kb + SKEYS - 1) / SKEYS) : 0) : 0;
     const int nst = Q8 ? n_cst + ((p.nsplit == 1 || last_split) ? (S + SKEYS - 1) / SKEYS : 0)
                        : (ke > kb ? (int)((ke - kb + SKEYS - 1) / SKEYS) : 0);
-    const int my_n = nst > wave ? (nst - wave + 3) / 4 : 0;
+    // The split holding the new rows has one stage more than the others, and one
+    // wave would run it after everyone else's last stage.  When the new rows fit in
+    // that last stage, it is loaded in the prologue into wave 3's second slot
+    // (first used by wave 3's stage 1) and run before the loop by waves 0 .. NCT-1,
+    // one column tile each; the loop then runs the other nst - 1 stages.
+    const bool sfx_split = !Q8 && (p.nsplit == 1 || last_split) && nst >= 2 &&
+                           kb + (int64_t)SKEYS * (nst - 1) <= npre;
+    const int nmain = sfx_split ? nst - 1 : nst;
+    const int my_n = nmain > wave ? (nmain - wave + 3) / 4 : 0;
     auto is_q8 = [&](int t) { return Q8 && wave + 4 * t < n_cst; };
 
     const int64_t nstride_b = (int64_t)p.n_kv_heads * ROWB;
@@ -234,9 +242,7 @@ __global__ __launch_bounds__(THREADS) void attn_cont_kernel(const AttnParams p) 
     const uint64_t kc_a = (uint64_t)(uintptr_t)kc0, vc_a = (uint64_t)(uintptr_t)vc0;
     const uint64_t kn_a = (uint64_t)(uintptr_t)kn0, vn_a = (uint64_t)(uintptr_t)vn0;
     const uint32_t ring_lds = (uint32_t)(wave * RING);
-    auto load_stage = [=](int t) {
-        const int i_st = wave + 4 * t;
-        const unsigned char *kd = smem + ring_lds + (t % NSW) * STAGE;
+    auto load_stage_to = [=](int i_st, const unsigned char *kd) {
         const unsigned char *vd = kd + HALF;
         if (Q8 && i_st < n_cst) {
             const int64_t key0 = kb + (int64_t)i_st * SKEYS;                   // a multiple of 32
@@ -271,6 +277,8 @@ __global__ __launch_bounds__(THREADS) void attn_cont_kernel(const AttnParams p) 
             }
         }
     };
+    auto load_stage = [=](int t) { load_stage_to(wave + 4 * t, smem + ring_lds + (t % NSW) * STAGE); };
+    const unsigned char *sfx_lds = smem + 3 * RING + STAGE;   // the split suffix stage: wave 3's slot 1
 
     // ---- read maps (per lane, loop invariant): K fragments and transposing V reads of the swizzled rows
     uint32_t ka[D / 16];
@@ -315,6 +323,7 @@ __global__ __launch_bounds__(THREADS) void attn_cont_kernel(const AttnParams p) 
             dma16((const void *)src, qlds + base * ROWB);
         }
     }
+    if (sfx_split && wave == 3) load_stage_to(nst - 1, sfx_lds);
     if (my_n > 0) {
         load_stage(0);
         if (is_q8(0)) wait_vmcnt<LOADS_Q8>();
@@ -322,7 +331,7 @@ __global__ __launch_bounds__(THREADS) void attn_cont_kernel(const AttnParams p) 
     } else {
         wait_vmcnt<0>();
     }
-    __builtin_amdgcn_s_barrier();       // all of Q is in LDS
+    __builtin_amdgcn_s_barrier();       // all of Q (and the split suffix stage) is in LDS
     asm volatile("" ::: "memory");
 
     bool o_scaled = !Q8;                // Q8: cached part of O still in code units of V
@@ -338,33 +347,17 @@ __global__ __launch_bounds__(THREADS) void attn_cont_kernel(const AttnParams p) 
 
     // one stage; the kind (int8 codes or bf16 rows) is a compile-time tag, so the
     // int8 stages and the bf16 stages run in loops of their own
-    auto stage = [&](auto kind, int t) {
+    // the arithmetic of one stage for the column tiles in CM (a bit mask)
+    auto compute = [&](auto kind, auto cm, const unsigned char *ks_, const unsigned char *vs_,
+                       int64_t key0) {
         constexpr bool q8 = decltype(kind)::value;
-        asm volatile("" ::: "memory");
-        if (t + 1 < my_n) {
-            load_stage(t + 1);          // its slot held stage t-1, consumed last iteration
-            if (is_q8(t + 1)) wait_vmcnt<LOADS_Q8>();   // stage t landed, stage t+1 in flight
-            else wait_vmcnt<LOADS>();
-        } else {
-            wait_vmcnt<0>();
-        }
-        asm volatile("" ::: "memory");
-        const int i_st = wave + 4 * t;
-        // absolute key of the stage's first row
-        const int64_t key0 = Q8 ? (q8 ? kb + (int64_t)i_st * SKEYS : npre + (int64_t)(i_st - n_cst) * SKEYS)
-                                : kb + (int64_t)i_st * SKEYS;
-        const unsigned char *ks_ = smem + ring_lds + (t % NSW) * STAGE;
-        const unsigned char *vs_ = ks_ + HALF;
-        if constexpr (Q8 && !q8) {
-            if (!o_scaled) scale_o();
-        }
-
+        constexpr int CM = decltype(cm)::value;
         // S^T for every column tile: each K fragment feeds NCT chains
         f32x16 s[NCT];
 #pragma unroll
         for (int c = 0; c < NCT; ++c)
 #pragma unroll
-            for (int i = 0; i < 16; ++i) s[c][i] = 0.f;
+            for (int i = 0; i < 16; ++i) s[c][i] = 0.f;   // unused tiles: dead code
         if constexpr (q8) {
             // lane (j, grp): codes of row j, head-dim steps 2 pr and 2 pr + 1
 #pragma unroll
@@ -374,6 +367,7 @@ __global__ __launch_bounds__(THREADS) void attn_cont_kernel(const AttnParams p) 
                 codes_to_bf16(w, a0, a1);
 #pragma unroll
                 for (int c = 0; c < NCT; ++c) {
+                    if (!((CM >> c) & 1)) continue;
                     const u32x4 b0 = *(const u32x4 *)(qlds + 32 * c * ROWB + ka[2 * pr]);
                     const u32x4 b1 = *(const u32x4 *)(qlds + 32 * c * ROWB + ka[2 * pr + 1]);
                     s[c] = E::mfma(a0, b0, s[c]);
@@ -386,6 +380,7 @@ __global__ __launch_bounds__(THREADS) void attn_cont_kernel(const AttnParams p) 
                 const u32x4 a = *(const u32x4 *)(ks_ + ka[ks]);
 #pragma unroll
                 for (int c = 0; c < NCT; ++c) {
+                    if (!((CM >> c) & 1)) continue;
                     // Q row 32*c + j has the same swizzle as row j
                     const u32x4 b = *(const u32x4 *)(qlds + 32 * c * ROWB + ka[ks]);
                     s[c] = E::mfma(a, b, s[c]);
@@ -396,6 +391,7 @@ __global__ __launch_bounds__(THREADS) void attn_cont_kernel(const AttnParams p) 
         u32x4 pf[NCT][2];
 #pragma unroll
         for (int c = 0; c < NCT; ++c) {
+            if (!((CM >> c) & 1)) continue;
             // mask: keys past a row's causal bound (new rows) or past the cached
             // prefix (an int8 stage reaching beyond npre)
             if (key0 + SKEYS > npre + 1 || (q8 && key0 + SKEYS > npre)) {
@@ -444,6 +440,7 @@ __global__ __launch_bounds__(THREADS) void attn_cont_kernel(const AttnParams p) 
                 codes_to_bf16(w, a0, a1);
 #pragma unroll
                 for (int c = 0; c < NCT; ++c) {
+                    if (!((CM >> c) & 1)) continue;
                     rs[c].o[mt] = E::mfma(a0, pf[c][0], rs[c].o[mt]);
                     rs[c].o[mt] = E::mfma(a1, pf[c][1], rs[c].o[mt]);
                 }
@@ -462,10 +459,48 @@ __global__ __launch_bounds__(THREADS) void attn_cont_kernel(const AttnParams p) 
                     const u32x4 a = {lo2[0], lo2[1], hi2[0], hi2[1]};
 #pragma unroll
                     for (int c = 0; c < NCT; ++c)
-                        rs[c].o[mt] = E::mfma(a, pf[c][kk], rs[c].o[mt]);
+                        if ((CM >> c) & 1) rs[c].o[mt] = E::mfma(a, pf[c][kk], rs[c].o[mt]);
                 }
         }
     };
+    auto stage = [&](auto kind, int t) {
+        constexpr bool q8 = decltype(kind)::value;
+        asm volatile("" ::: "memory");
+        if (t + 1 < my_n) {
+            load_stage(t + 1);          // its slot held stage t-1, consumed last iteration
+            if (is_q8(t + 1)) wait_vmcnt<LOADS_Q8>();   // stage t landed, stage t+1 in flight
+            else wait_vmcnt<LOADS>();
+        } else {
+            wait_vmcnt<0>();
+        }
+        asm volatile("" ::: "memory");
+        const int i_st = wave + 4 * t;
+        // absolute key of the stage's first row
+        const int64_t key0 = Q8 ? (q8 ? kb + (int64_t)i_st * SKEYS : npre + (int64_t)(i_st - n_cst) * SKEYS)
+                                : kb + (int64_t)i_st * SKEYS;
+        const unsigned char *ks_ = smem + ring_lds + (t % NSW) * STAGE;
+        const unsigned char *vs_ = ks_ + HALF;
+        if constexpr (Q8 && !q8) {
+            if (!o_scaled) scale_o();
+        }
+        compute(kind, std::integral_constant<int, (1 << NCT) - 1>{}, ks_, vs_, key0);
+    };
+
+    // the split suffix stage, one column tile per wave (waves 0 .. NCT-1), then a
+    // barrier: after it wave 3 may refill its second slot
+    if (sfx_split) {
+        const int64_t key0 = kb + (int64_t)SKEYS * (nst - 1);
+        if (wave == 0) compute(std::false_type{}, std::integral_constant<int, 1>{}, sfx_lds, sfx_lds + HALF, key0);
+        if constexpr (NCT > 1) {
+            if (wave == 1) compute(std::false_type{}, std::integral_constant<int, 2>{}, sfx_lds, sfx_lds + HALF, key0);
+        }
+        if constexpr (NCT > 2) {
+            if (wave == 2) compute(std::false_type{}, std::integral_constant<int, 4>{}, sfx_lds, sfx_lds + HALF, key0);
+        }
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");
+    }
     int t = 0;
     if constexpr (Q8) {
         for (; t < my_n && is_q8(t); ++t) stage(std::true_type{}, t);
