@@ -79,7 +79,20 @@ Split plan_split(const kvr_desc *d, int64_t L_prefix, int64_t S) {
     if (want <= 1) return s;
     int64_t chunk = (L_prefix + want - 1) / want;
     chunk = (chunk + kKeyTile - 1) / kKeyTile * kKeyTile;
-    const int64_t n = (L_prefix + chunk - 1) / chunk;
+    int64_t n = (L_prefix + chunk - 1) / chunk;
+    // A prefix up to 32 - S keys past a multiple of want x 128 keys (a decode
+    // chain just past a round length) would round every chunk above up by 64 keys,
+    // and two of the four waves of the keys-split kernel would run one stage more.
+    // Instead: want chunks of a multiple of 128 keys, the last one taking the
+    // remainder; its few extra keys share the stage of the new rows, which that
+    // kernel runs across its waves.  Every wave then runs the same stage count.
+    if (use_cont(d, S) && S <= 32) {
+        const int64_t c2 = L_prefix / want / 128 * 128;
+        if (c2 >= kMinSplitKeys && L_prefix - want * c2 + S <= 32) {
+            chunk = c2;
+            n = want;
+        }
+    }
     if (n <= 1) return s;
     s.nsplit = (int32_t)n;
     s.chunk = chunk;

@@ -373,3 +373,28 @@ def test_full_size_sampled(L):
     assert maxabs(full[rows], want) <= TOL[torch.bfloat16]
     want_c, _ = ref.prefill(q, k, v, rows=list(range(L, n)))
     assert maxabs(cont, want_c) <= TOL[torch.bfloat16]
+
+
+# ------------------------------------- prefixes just past a round length (split plan)
+@pytest.mark.parametrize("L,S", [(32768 + 5, 1), (32768 + 30, 1), (32768 + 5, 24), (16384 + 3, 24), (16384 + 7, 1)])
+def test_prefix_just_past_round_length(L, S):
+    """Prefixes a few keys past a multiple of the split count x 128 keys: the last split
+    takes the extra prefix keys with the new rows (the plan a decode chain hits on every
+    step after the first).  Continuation and continuation + cache update against the
+    oracle and against the GPU prefill rows; the updated cache rows are exact copies."""
+    n = L + S
+    say("prefix just past a round length L=%d S=%d" % (L, S))
+    sh = W.QWEN
+    q, k, v = W.qkv(n, sh, seed=L + S)
+    full, _, _, _ = gpu_prefill(sh, q, k, v)
+    _, kc, vc, d = gpu_prefill(sh, q[:L], k[:L], v[:L], capacity=n)
+    cont = gpu_continue(d, q[L:], k[L:], v[L:], kc, vc, L)
+    qs, ks, vs = dev(q[L:], k[L:], v[L:])
+    out2 = torch.empty_like(qs)
+    kvr.kvr_continue_append(d, qs, ks, vs, kc, vc, L, S, out2, kvr.workspace_for(d, L, S))
+    torch.cuda.synchronize()
+    assert torch.equal(cont, out2)
+    assert torch.equal(kc[:, L:n].cpu(), k[L:].transpose(0, 1)) and torch.equal(vc[:, L:n].cpu(), v[L:].transpose(0, 1))
+    assert float((cont - full[L:]).abs().max()) <= CLAIM1_TOL
+    want, _ = ref.prefill(q, k, v, rows=list(range(L, n)))
+    assert maxabs(cont, want) <= TOL[torch.bfloat16]
