@@ -376,7 +376,8 @@ def test_full_size_sampled(L):
 
 
 # ------------------------------------- prefixes just past a round length (split plan)
-@pytest.mark.parametrize("L,S", [(32768 + 5, 1), (32768 + 30, 1), (32768 + 5, 24), (16384 + 3, 24), (16384 + 7, 1)])
+@pytest.mark.parametrize("L,S", [(32768 + 5, 1), (32768 + 30, 1), (32768 + 5, 24), (32768 + 3, 12), (16384 + 3, 24),
+                                 (16384 + 7, 1)])
 def test_prefix_just_past_round_length(L, S):
     """Prefixes a few keys past a multiple of the split count x 128 keys: the last split
     takes the extra prefix keys with the new rows (the plan a decode chain hits on every

@@ -137,7 +137,8 @@ def test_prefill_rope(Hq, Hkv, D, L, dt):
 @pytest.mark.parametrize("Lp,S,dt", [(1000, 24, torch.bfloat16), (3774, 24, torch.bfloat16),
                                      (900, 1, torch.bfloat16), (20000, 24, torch.bfloat16),
                                      (300, 40, torch.bfloat16), (0, 7, torch.bfloat16),
-                                     (1000, 24, torch.float16), (200, 9, torch.float32)])
+                                     (1000, 24, torch.float16), (200, 9, torch.float32),
+                                     (32768 + 6, 1, torch.bfloat16), (32768 + 2, 12, torch.float16)])
 def test_continue_rope(Lp, S, dt):
     say("continue rope Lp=%d S=%d %s" % (Lp, S, dt))
     Hq, Hkv, D = (32, 8, 128) if dt != torch.float32 else (4, 2, 64)
