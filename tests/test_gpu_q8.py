@@ -114,6 +114,7 @@ def run_q8(desc, L_art, Lp, S, seed, rows=None):
 
 @pytest.mark.parametrize("Lp,S,extra", [
     (1, 1, 0), (100, 24, 0), (1000, 1, 7), (3774, 24, 0), (3774, 3, 40), (5000, 17, 0), (257, 24, 1),
+    (32768 + 5, 1, 0), (32768 + 2, 24, 9),      # prefixes just past a round length (last split takes the extra keys)
 ])
 def test_continue_q8_matches_oracle(Lp, S, extra):
     say("continue_q8: Lp %d S %d artifact %d" % (Lp, S, Lp + extra))
