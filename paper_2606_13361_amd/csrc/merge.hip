@@ -4,9 +4,10 @@
 //   M = max_s m_s,  w_s = 2^(m_s - M),  out = sum_s w_s O_s / sum_s w_s l_s
 // which is the log-sum-exp merge of partial softmax sums.
 //
-// One lane per 4 consecutive head-dim values of one row: a 256-lane
-// workgroup covers 256 / (D/4) rows of one kv head (8 at D = 128, 16 at
-// D = 64).  The lanes of a row first build the split weights together --
+// One lane per 4 consecutive head-dim values of one row: a 64-lane
+// workgroup covers 64 / (D/4) rows of one kv head (2 at D = 128, 4 at
+// D = 64), so the partials of a continuation are read by many compute units
+// at once.  The lanes of a row first build the split weights together --
 // lane k takes splits k, k + D/4, ...; the row maximum and l come from xor
 // butterflies inside the row's lanes (same bits in every lane); the weights
 // go through LDS -- then every lane streams its 16 bytes of every split with
@@ -20,7 +21,7 @@ namespace {
 
 using namespace dev;
 
-constexpr int MERGE_THREADS = 256;
+constexpr int MERGE_THREADS = 64;
 constexpr int MERGE_BATCH = 16;   // split loads in flight per lane
 
 template <int D, class E>
