@@ -16,13 +16,18 @@
 #include "kvr_internal.hpp"
 
 static int g_launches = 0;
+static int64_t g_nsplit = -1, g_chunk = -1;   // the split plan the last continuation launch got
 
 namespace kvr {
 hipError_t launch_attn_bf16(const AttnParams &, int, int, bool, int, hipStream_t) { ++g_launches; return hipErrorUnknown; }
 hipError_t launch_merge_bf16(const MergeParams &, int, bool, hipStream_t) { ++g_launches; return hipErrorUnknown; }
 hipError_t launch_attn_pp(const AttnParams &, int, bool, int, hipStream_t) { ++g_launches; return hipErrorUnknown; }
-hipError_t launch_attn_rows(const AttnParams &, bool, int, hipStream_t) { ++g_launches; return hipErrorUnknown; }
-hipError_t launch_attn_cont(const AttnParams &, int, bool, bool, int, hipStream_t) { ++g_launches; return hipErrorUnknown; }
+hipError_t launch_attn_rows(const AttnParams &p, bool, int, hipStream_t) {
+    ++g_launches; g_nsplit = p.nsplit; g_chunk = p.chunk; return hipErrorUnknown;
+}
+hipError_t launch_attn_cont(const AttnParams &p, int, bool, bool, int, hipStream_t) {
+    ++g_launches; g_nsplit = p.nsplit; g_chunk = p.chunk; return hipErrorUnknown;
+}
 hipError_t launch_quantize(const QuantParams &, hipStream_t) { ++g_launches; return hipErrorUnknown; }
 hipError_t launch_attn_f32(const AttnParams &, int, int, hipStream_t) { ++g_launches; return hipErrorUnknown; }
 hipError_t launch_append(const AppendParams &, hipStream_t) { ++g_launches; return hipErrorUnknown; }
@@ -193,6 +198,40 @@ static void fuzz() {
     }
 }
 
+// The split plan of the continuation, as the kernels receive it: splits of
+// whole 64-key tiles, no more splits than 256-key pieces of the prefix, the
+// last one non-empty and
+// ending at the prefix end -- or, for a prefix at most 32 - S keys past a
+// multiple of the split count x 128 keys, chunks of a multiple of 128 keys
+// whose last split also takes the few remaining keys.
+static void split_plans() {
+    const int64_t cap = 40200;
+    kvr_desc e = desc(32, 8, 128, KVR_BF16, cap);
+    void *P = (void *)(uintptr_t)0x100000;
+    const int64_t lens[] = {256, 300, 1000, 3774, 4096, 8191, 16384, 16387, 16400, 32768, 32769, 32775,
+                            32790, 32799, 32800, 32900, 40000};
+    const int64_t sfx[] = {1, 2, 8, 12, 24, 31, 32, 33, 64, 96};
+    int planned = 0;
+    for (int64_t L : lens)
+        for (int64_t S : sfx) {
+            if (L + S > cap) continue;
+            const size_t ws = kvr_workspace_bytes(&e, L, S, 1);
+            g_nsplit = g_chunk = -1;
+            const int st = kvr_continue(&e, P, P, P, P, P, L, S, P, P, ws, nullptr);
+            if (st != KVR_ERR_DEVICE) { fprintf(stderr, "plan L=%ld S=%ld: status %d\n", (long)L, (long)S, st); ++fails; continue; }
+            if (g_nsplit <= 1) continue;
+            ++planned;
+            const int64_t n = g_nsplit, c = g_chunk;
+            const bool tiles = c % 64 == 0 && n <= (L + 255) / 256 && (n - 1) * c < L;
+            const bool covers = n * c >= L || (c % 128 == 0 && L - n * c + S <= 32);
+            if (!tiles || !covers) {
+                fprintf(stderr, "plan L=%ld S=%ld: %ld splits of %ld keys\n", (long)L, (long)S, (long)n, (long)c);
+                ++fails;
+            }
+        }
+    if (planned < 50) { fprintf(stderr, "only %d split plans checked\n", planned); ++fails; }
+}
+
 int main() {
     if (kvr_abi_version() != KVR_ABI_VERSION) {
         fprintf(stderr, "ABI version mismatch\n");
@@ -201,6 +240,7 @@ int main() {
     for (int s = -1; s < 12; ++s)
         if (!kvr_strerror(s) || !kvr_strerror(s)[0]) ++fails;
     fixed_cases();
+    split_plans();
     fuzz();
     if (fails) {
         fprintf(stderr, "%d checks failed\n", fails);
