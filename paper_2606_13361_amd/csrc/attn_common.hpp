@@ -43,6 +43,15 @@ constexpr float kRescaleSlack = 8.f;
 // A lane's weights of one tile summing to at most 2^kRescaleSlack are each at
 // most that: the test that lets a tile skip the row maximum.
 constexpr float kSlackSum = 256.f;
+// A tile whose weights (against the current reference) sum above this share
+// of the row's running sum is "significant": if it also holds a new row
+// maximum, the reference moves to that maximum exactly, so the tile's largest
+// weight is 2^0 = 1, which the 16-bit P operand holds without rounding.  Only
+// weights of at most a quarter of the running sum (or below the reference,
+// as in a plain running maximum) are ever rounded, so a dominant key of a
+// peaky row is never.  On flat rows only the first few tiles of a key range
+// are significant.
+constexpr float kSignificance = 0.25f;
 
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
     // v_cvt_pk_bf16_f32: round to nearest even
@@ -149,6 +158,9 @@ __device__ __forceinline__ float pair_sum(float x) {
     const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
     return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
+// true in both lanes of a row when it holds in either
+__device__ __forceinline__ bool pair_any(bool b) { return pair_max(b ? 1.f : 0.f) > 0.f; }
+
 
 // Locate the segment (reader) that owns a linear row-tile index.
 __device__ __forceinline__ int find_segment(const AttnParams &p, int tile) {
@@ -210,6 +222,19 @@ struct RowState {
             for (int i = 0; i < 16; ++i) o[mt][i] = 0.f;
     }
 };
+
+// Move the reference of a lane's row to m_new (>= the current one): (O, l)
+// are rescaled by 2^(m - m_new).
+template <int D>
+__device__ __forceinline__ void move_reference(RowState<D> &rs, float m_new) {
+    const float alpha = __builtin_amdgcn_exp2f(rs.m - m_new);
+    rs.m = m_new;
+    rs.l *= alpha;
+#pragma unroll
+    for (int mt = 0; mt < D / 32; ++mt)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) rs.o[mt][i] *= alpha;
+}
 
 // Direct-to-LDS load of 16 bytes per lane: lane l's bytes land at LDS byte
 // lds + 16*l (lds is wave-uniform).  Issued as inline asm so the compiler does
@@ -318,30 +343,34 @@ __device__ __forceinline__ void tile_step(RowState<D> &rs, const u32x4 (&qf)[D /
 #pragma unroll
         for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s[st][i]);
     mx = pair_max(mx) * c2;
-    // lazy rescale: move the reference only when p could exceed 2^kRescaleSlack
+    // lazy rescale: move the reference when p could exceed 2^kRescaleSlack
+    // (the first tile always)
     const bool need = mx > rs.m + kRescaleSlack;
-    if (__ballot(need)) {
-        const float m_new = need ? mx : rs.m;
-        const float alpha = __builtin_amdgcn_exp2f(rs.m - m_new);
-        rs.m = m_new;
-        rs.l *= alpha;
-#pragma unroll
-        for (int mt = 0; mt < D / 32; ++mt)
-#pragma unroll
-            for (int i = 0; i < 16; ++i) rs.o[mt][i] *= alpha;
-    }
-    float lsum = 0.f;
+    if (__ballot(need)) move_reference(rs, need ? mx : rs.m);
     u32x4 pf[NSUB][2];   // P^T as bf16, [sub-tile][16-key half]
+    auto exps = [&]() {
+        float lsum = 0.f;
 #pragma unroll
-    for (int st = 0; st < NSUB; ++st) {
+        for (int st = 0; st < NSUB; ++st) {
 #pragma unroll
-        for (int i = 0; i < 16; i += 2) {
-            const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[st][i], c2, -rs.m));
-            const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[st][i + 1], c2, -rs.m));
-            const uint32_t pk = E::pack2(p0, p1);
-            // row sum in fp32 adds (a v_dot2 would wait behind MFMAs on the matrix pipe)
-            lsum += p0 + p1;
-            pf[st][i >> 3][(i & 7) >> 1] = pk;
+            for (int i = 0; i < 16; i += 2) {
+                const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[st][i], c2, -rs.m));
+                const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[st][i + 1], c2, -rs.m));
+                const uint32_t pk = E::pack2(p0, p1);
+                // row sum in fp32 adds (a v_dot2 would wait behind MFMAs on the matrix pipe)
+                lsum += p0 + p1;
+                pf[st][i >> 3][(i & 7) >> 1] = pk;
+            }
+        }
+        return lsum;
+    };
+    float lsum = exps();
+    // a significant tile with a new maximum: reference to that maximum, exactly
+    if (__ballot(mx > rs.m && lsum > kSignificance * rs.l)) {
+        const bool mv = mx > rs.m && pair_any(lsum > kSignificance * rs.l);
+        if (__ballot(mv)) {
+            move_reference(rs, mv ? mx : rs.m);
+            lsum = exps();
         }
     }
     rs.l += lsum;

@@ -407,25 +407,29 @@ __global__ __launch_bounds__(THREADS) void attn_cont_kernel(const AttnParams p) 
 #pragma unroll
             for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s[c][i]);
             mx = pair_max(mx) * c2s;
+            // the first stage, or p could exceed 2^kRescaleSlack
             const bool need = mx > rs[c].m + kRescaleSlack;
-            if (__ballot(need)) {
-                const float m_new = need ? mx : rs[c].m;
-                const float alpha = __builtin_amdgcn_exp2f(rs[c].m - m_new);
-                rs[c].m = m_new;
-                rs[c].l *= alpha;
+            if (__ballot(need)) move_reference(rs[c], need ? mx : rs[c].m);
+            auto exps = [&]() {
+                float lsum = 0.f;
 #pragma unroll
-                for (int mt = 0; mt < D / 32; ++mt)
-#pragma unroll
-                    for (int i = 0; i < 16; ++i) rs[c].o[mt][i] *= alpha;
-            }
-            float lsum = 0.f;
-#pragma unroll
-            for (int i = 0; i < 16; i += 2) {
-                const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[c][i], c2s, -rs[c].m));
-                const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[c][i + 1], c2s, -rs[c].m));
-                const uint32_t pk = E::pack2(p0, p1);
-                lsum += p0 + p1;
-                pf[c][i >> 3][(i & 7) >> 1] = pk;
+                for (int i = 0; i < 16; i += 2) {
+                    const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[c][i], c2s, -rs[c].m));
+                    const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[c][i + 1], c2s, -rs[c].m));
+                    const uint32_t pk = E::pack2(p0, p1);
+                    lsum += p0 + p1;
+                    pf[c][i >> 3][(i & 7) >> 1] = pk;
+                }
+                return lsum;
+            };
+            float lsum = exps();
+            // a significant stage with a new maximum: reference to it, exactly
+            if (__ballot(mx > rs[c].m && lsum > kSignificance * rs[c].l)) {
+                const bool mv = mx > rs[c].m && pair_any(lsum > kSignificance * rs[c].l);
+                if (__ballot(mv)) {
+                    move_reference(rs[c], mv ? mx : rs[c].m);
+                    lsum = exps();
+                }
             }
             rs[c].l += lsum;
         }

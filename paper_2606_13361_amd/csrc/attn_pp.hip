@@ -6,7 +6,7 @@
 // group A, waves 4-7 group B; the two waves sharing a SIMD belong to
 // different groups.  Per 64-key tile t a group runs two steps:
 //   GEMM(t)  O += V_{t-1} P_{t-1}  and  S_t = K_t Q^T     (32 MFMAs)
-//   SOFT(t)  mask, row max, lazy rescale, P_t = exp2(...) (VALU)
+//   SOFT(t)  mask, row max, rescale, P_t = exp2(...)        (VALU)
 // and the groups are offset by one step: while A runs GEMM(t), B runs
 // SOFT(t-1); while A runs SOFT(t), B runs GEMM(t).  Every step ends at a
 // workgroup barrier, so each SIMD always has one wave feeding the matrix core
@@ -288,8 +288,9 @@ __global__ __launch_bounds__(PP_THREADS) void attn_pp_kernel(const AttnParams p)
         }
         // P against the current reference m first; the row maximum is needed
         // only when some lane's weights sum above 2^kRescaleSlack (then one of
-        // them may exceed it) -- the first tile (m = -1e30) always, later tiles
-        // almost never
+        // them may exceed it) or above kSignificance of the running sum (a
+        // significant tile: a new maximum there becomes the reference exactly)
+        // -- the first tile (m = -1e30) always, on flat rows the next few
         auto exps = [&](auto loads) {
             float lsum[4] = {0.f, 0.f, 0.f, 0.f};   // four independent partial sums
 #pragma unroll
@@ -311,7 +312,7 @@ __global__ __launch_bounds__(PP_THREADS) void attn_pp_kernel(const AttnParams p)
             return (lsum[0] + lsum[1]) + (lsum[2] + lsum[3]);
         };
         float part = exps(with_loads);
-        if (__ballot(!(part <= kSlackSum))) {
+        if (__ballot(!(part <= kSlackSum) || part > kSignificance * rs.l)) {
             // row max as a tree (5 dependent levels)
             float v[32];
 #pragma unroll
@@ -324,16 +325,10 @@ __global__ __launch_bounds__(PP_THREADS) void attn_pp_kernel(const AttnParams p)
 #pragma unroll
                 for (int i = 0; i < w; ++i) v[i] = fmaxf(v[i], v[i + w]);
             const float mx = pair_max(v[0]) * c2;
-            const bool need = mx > rs.m + kRescaleSlack;
+            const bool sig = pair_any(part > kSignificance * rs.l);
+            const bool need = mx > rs.m + (sig ? 0.f : kRescaleSlack);
             if (__ballot(need)) {
-                const float m_new = need ? mx : rs.m;
-                const float alpha = __builtin_amdgcn_exp2f(rs.m - m_new);
-                rs.m = m_new;
-                rs.l *= alpha;
-#pragma unroll
-                for (int mt = 0; mt < D / 32; ++mt)
-#pragma unroll
-                    for (int i = 0; i < 16; ++i) rs.o[mt][i] *= alpha;
+                move_reference(rs, need ? mx : rs.m);
                 part = exps(std::false_type{});
             }
         }

@@ -190,7 +190,8 @@ __global__ __launch_bounds__(RTHREADS) void attn_rows_kernel(const AttnParams p)
     // come from two independent accumulation chains (even / odd head-dim
     // steps).  Softmax as in the two-group kernel: weights against the current
     // reference m first, the row maximum only when some lane's weights sum
-    // above 2^kRescaleSlack (the first stage always, later ones almost never).
+    // above 2^kRescaleSlack or above kSignificance of the running sum (the
+    // first stage always, on flat rows the next few).
     auto stage_step = [&](const unsigned char *ks_, const unsigned char *vs_, bool mask, int lim) {
         u32x4 kf[D / 16], vf[8];
 #pragma unroll
@@ -235,21 +236,15 @@ __global__ __launch_bounds__(RTHREADS) void attn_rows_kernel(const AttnParams p)
             return ls[0] + ls[1];
         };
         float part = exps();
-        if (__ballot(!(part <= kSlackSum))) {
+        if (__ballot(!(part <= kSlackSum) || part > kSignificance * rs.l)) {
             float mx = sv[0];
 #pragma unroll
             for (int i = 1; i < 16; ++i) mx = fmaxf(mx, sv[i]);
             mx = pair_max(mx) * c2;
-            const bool need = mx > rs.m + kRescaleSlack;
+            const bool sig = pair_any(part > kSignificance * rs.l);
+            const bool need = mx > rs.m + (sig ? 0.f : kRescaleSlack);
             if (__ballot(need)) {
-                const float m_new = need ? mx : rs.m;
-                const float alpha = __builtin_amdgcn_exp2f(rs.m - m_new);
-                rs.m = m_new;
-                rs.l *= alpha;
-#pragma unroll
-                for (int mt = 0; mt < D / 32; ++mt)
-#pragma unroll
-                    for (int i = 0; i < 16; ++i) rs.o[mt][i] *= alpha;
+                move_reference(rs, need ? mx : rs.m);
                 part = exps();
             }
         }

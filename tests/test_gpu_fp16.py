@@ -162,3 +162,22 @@ def test_f16_is_closer_than_bf16():
         errs[dt] = maxabs(out, want)
     say("  max err bf16 %.3g, fp16 %.3g" % (errs[torch.bfloat16], errs[F16]))
     assert errs[F16] < errs[torch.bfloat16] / 2
+
+
+@pytest.mark.parametrize("Hq,Hkv,Lp,S", [(8, 2, 3000, 5), (16, 2, 2500, 3)])
+def test_continue_f16_head_dim_64_split(Hq, Hkv, Lp, S):
+    """head_dim 64 continuations with several key splits (the merge's
+    4-rows-per-workgroup geometry) in fp16: oracle and Claim 1."""
+    say("continue fp16 %d/%d/64 Lp=%d S=%d" % (Hq, Hkv, Lp, S))
+    sh = W.Shape(Hq, Hkv, 64, F16)
+    n = Lp + S
+    q, k, v = W.qkv(n, sh, seed=43 + Lp)
+    full, _, _, _ = prefill(sh, q, k, v)
+    _, kc, vc, d = prefill(sh, q[:Lp], k[:Lp], v[:Lp], cap=n)
+    assert kvr.kvr_workspace_bytes(d, Lp, S) > 0      # the plan splits the prefix
+    out = cont(d, q[Lp:], k[Lp:], v[Lp:], kc, vc, Lp)
+    torch.cuda.synchronize()
+    claim1(out, full[Lp:])
+    want, _ = ref.continue_(q[Lp:], k[Lp:], v[Lp:], k[:Lp].transpose(0, 1).contiguous(),
+                            v[:Lp].transpose(0, 1).contiguous(), Lp)
+    assert maxabs(out, want) <= TOL

@@ -205,12 +205,11 @@ def test_stress_softmax(kind):
     # allowance on top (and one bf16 ulp, |x| * 2^-7, between two GPU results).
     excess(full[rows], want, TOL[torch.bfloat16], 2.0 ** -8)
     excess(cont, want[-S:], TOL[torch.bfloat16], 2.0 ** -8)
-    # Between two GPU results also: the running maximum is moved lazily, so the
-    # largest softmax weight 2^d (0 < d <= 8) is itself rounded to bf16; with
-    # w its normalised weight that moves the output by at most
-    # 2^-9 * w (1 - w) * (max v - min v) <= 2^-11 * (max v - min v) in each result.
-    spread = float(v.float().max() - v.float().min())
-    excess(cont, full[Lp:].double().cpu().numpy(), CLAIM1_TOL + 2.0 ** -10 * spread, 2.0 ** -7)
+    # Claim 1 between two GPU results at the plain bar (2e-3 and one output
+    # ulp): a tile that holds a significant share of a row's weight and a new
+    # maximum moves the reference to that maximum exactly, so a dominant key's
+    # weight is 1 and never rounded in P.
+    claim1(cont, full[Lp:])
 
 
 def excess(gpu, want, tol, rel):
@@ -264,11 +263,13 @@ def test_decode_chain():
 
 
 def test_many_readers_batched():
-    """64 readers of one cached prefix, suffixes U[24, 256], in one call."""
-    say("many readers")
+    """64 readers of one cached 3774-token prefix, suffixes U[24, 256] (the
+    many-readers workload at full size), in one call: every row of every reader
+    against the oracle."""
+    say("many readers: 64 over a cached 3774-token prefix")
     sh = W.QWEN
-    Lp = 1200
-    lens = W.reader_lengths(n=64, seed=0)
+    Lp = W.READERS_L
+    lens = W.reader_lengths(n=W.READERS_N, seed=0)
     cu = W.cu_seqlens(lens)
     total = cu[-1]
     g = W.gen(21)
@@ -279,13 +280,16 @@ def test_many_readers_batched():
     out = torch.empty_like(qd)
     kvr.kvr_continue_batched(d, qd, kd, vd, cu, kc, vc, Lp, out)
     torch.cuda.synchronize()
+    got = out.cpu()
     kc_o, vc_o = kp.transpose(0, 1).contiguous(), vp.transpose(0, 1).contiguous()
-    for r in range(64):
+    worst = 0.0
+    for r in range(W.READERS_N):
         a, b = cu[r], cu[r + 1]
-        rows = None if r % 8 == 0 else [0, b - a - 1]
-        want, _ = ref.continue_(qs[a:b], ks[a:b], vs[a:b], kc_o, vc_o, Lp, rows=rows)
-        got = out[a:b] if rows is None else out[a:b][rows]
-        assert maxabs(got, want) <= TOL[torch.bfloat16], r
+        want, _ = ref.continue_(qs[a:b], ks[a:b], vs[a:b], kc_o, vc_o, Lp)
+        err = maxabs(got[a:b], want)
+        worst = max(worst, err)
+        assert err <= TOL[torch.bfloat16], (r, err)
+    say("  readers max |gpu - oracle| = %.5f" % worst)
     # each reader equals its own single continuation (rounding only)
     for r in (0, 17, 63):
         a, b = cu[r], cu[r + 1]
@@ -353,9 +357,22 @@ def test_closed_forms_on_gpu():
 
 
 # ------------------------------------------------- full-size workloads, sampled
+def sampled_prefill_rows(n, seed):
+    """Rows of an n-token prefill checked against the oracle at full size: the
+    first and last 128, every 64-token tile boundary +-1 (the prefill's row
+    tiles hold 64 tokens of a kv group, its key tiles 64 keys), and 256 drawn
+    at random; the last 128 include the ragged last tile."""
+    rows = set(range(min(128, n))) | set(range(max(0, n - 128), n))
+    for b in range(64, n, 64):
+        rows |= {b - 1, b, b + 1}
+    rows |= set(np.random.default_rng(seed).integers(0, n, 256).tolist())
+    return sorted(r for r in rows if 0 <= r < n)
+
+
 @pytest.mark.parametrize("L", [3774, 16384, 32768])
 def test_full_size_sampled(L):
-    """The layer workloads at full size: continuation rows all checked, prefill rows sampled."""
+    """The layer workloads at full size: continuation rows all checked, prefill
+    rows sampled (first/last 128, every tile boundary +-1, 256 random)."""
     S = 24
     n = L + S
     say("full size L=%d S=%d" % (L, S))
@@ -366,13 +383,31 @@ def test_full_size_sampled(L):
     cont = gpu_continue(d, q[L:], k[L:], v[L:], kc, vc, L)
     torch.cuda.synchronize()
     assert float((cont - full[L:]).abs().max()) <= CLAIM1_TOL
-    rng = np.random.default_rng(L)
-    rows = sorted(set([0, 1, 31, 32, 33, 63, 64, 65, n // 2, n // 2 + 1, L - 1]
-                      + rng.integers(0, L, 24).tolist()))
+    rows = sampled_prefill_rows(n, L)
+    say("  %d prefill rows against the oracle" % len(rows))
     want, _ = ref.prefill(q, k, v, rows=rows)
     assert maxabs(full[rows], want) <= TOL[torch.bfloat16]
     want_c, _ = ref.prefill(q, k, v, rows=list(range(L, n)))
     assert maxabs(cont, want_c) <= TOL[torch.bfloat16]
+
+
+@pytest.mark.parametrize("Hq,Hkv,Lp,S", [(8, 2, 3000, 5), (16, 2, 2500, 3), (8, 2, 4100, 24)])
+def test_continue_head_dim_64_split(Hq, Hkv, Lp, S):
+    """head_dim 64 continuations whose split plan has several key splits (the
+    merge's 4-rows-per-workgroup geometry): oracle and Claim 1."""
+    say("continue bf16 %d/%d/64 Lp=%d S=%d" % (Hq, Hkv, Lp, S))
+    sh = W.Shape(Hq, Hkv, 64, torch.bfloat16)
+    n = Lp + S
+    q, k, v = W.qkv(n, sh, seed=31 + Lp)
+    full, _, _, _ = gpu_prefill(sh, q, k, v)
+    _, kc, vc, d = gpu_prefill(sh, q[:Lp], k[:Lp], v[:Lp], capacity=n)
+    assert kvr.kvr_workspace_bytes(d, Lp, S) > 0     # the plan splits the prefix
+    cont = gpu_continue(d, q[Lp:], k[Lp:], v[Lp:], kc, vc, Lp)
+    torch.cuda.synchronize()
+    claim1(cont, full[Lp:])
+    want, _ = ref.continue_(q[Lp:], k[Lp:], v[Lp:], k[:Lp].transpose(0, 1).contiguous(),
+                            v[:Lp].transpose(0, 1).contiguous(), Lp)
+    assert maxabs(cont, want) <= TOL[torch.bfloat16]
 
 
 # ------------------------------------- prefixes just past a round length (split plan)

@@ -138,3 +138,45 @@ def test_logits_tied_head():
     lg = LO.logits(h, w, E, 1e-6)
     x = h / np.sqrt(np.mean(h * h) + 1e-6) * w
     np.testing.assert_allclose(lg, [float(np.dot(x, E[i])) for i in range(50)], rtol=1e-12)
+
+
+def _mlp_only(seed, gate_sign):
+    """A layer whose attention adds nothing (zero output projection) and whose
+    MLP input is positive: h > 0 and ln2 > 0 give x = rmsnorm(h) * ln2 > 0, so
+    gate rows with entries of one sign make every gate value x.Wg of that sign
+    and far from 0."""
+    W = weights(seed, zero=("wo",))
+    g = np.random.default_rng(seed + 100)
+    H, I = SH["hidden"], SH["intermediate"]
+    W["ln2"] = 0.5 + g.random(H)                                  # positive, not 1
+    W["wgu"][:I] = gate_sign * (2.0 + g.random((I, H)))           # gate rows: |x.Wg| >> 1
+    h = 0.2 + g.random((6, H))
+    return W, h
+
+
+def test_mlp_with_open_gate_is_the_product():
+    """silu(g) = g for g >> 0, so the MLP term is (x Wg^T * x Wu^T) Wd^T with
+    x = rmsnorm(h) * ln2 and the fused weight's rows gate | up, written out by
+    hand here.  Swapping gate and up (silu on the up half), dropping ln2, or
+    adding to anything but the residual stream all fail it."""
+    W, h = _mlp_only(7, +1.0)
+    I = SH["intermediate"]
+    out, _, _ = LO.layer(h, W, SH, None, None, 0)
+    x = h / np.sqrt(np.mean(h * h, axis=1, keepdims=True) + SH["eps"]) * W["ln2"]
+    gate = x @ W["wgu"][:I].T
+    up = x @ W["wgu"][I:].T
+    assert gate.min() > 40.0                                      # silu(gate) = gate to 1e-16
+    assert (up < 0).any() and (up > 0).any()                      # up is not one-signed
+    want = h + (gate * up) @ W["wd"].T
+    np.testing.assert_allclose(out, want, rtol=1e-12, atol=1e-10)
+    # the swapped reading (silu applied to the up half) is far from it
+    swapped = h + (LO.silu(up) * gate) @ W["wd"].T
+    assert np.max(np.abs(swapped - want)) > 1.0
+
+
+def test_mlp_with_closed_gate_vanishes():
+    """silu(g) = 0 for g << 0: the layer returns its input (attention adds
+    nothing either), whatever the up and down weights are."""
+    W, h = _mlp_only(8, -1.0)
+    out, _, _ = LO.layer(h, W, SH, None, None, 0)
+    np.testing.assert_allclose(out, h, rtol=0, atol=1e-12)
