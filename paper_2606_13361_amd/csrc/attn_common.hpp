@@ -52,6 +52,11 @@ constexpr float kSlackSum = 256.f;
 // peaky row is never.  On flat rows only the first few tiles of a key range
 // are significant.
 constexpr float kSignificance = 0.25f;
+// The first tiles (stages) of a key range are significant on almost every
+// row (a tile's weights are about 1/t of the running sum at tile t), so there
+// the kernels take the row maximum before the weights and move the reference
+// to every new maximum, instead of computing the weights twice.
+constexpr int kExactTiles = 5;
 
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
     // v_cvt_pk_bf16_f32: round to nearest even

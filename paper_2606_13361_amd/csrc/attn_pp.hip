@@ -311,8 +311,20 @@ __global__ __launch_bounds__(PP_THREADS) void attn_pp_kernel(const AttnParams p)
                 }
             return (lsum[0] + lsum[1]) + (lsum[2] + lsum[3]);
         };
+        const bool early = t < kExactTiles;
+        if (early) {
+            // a plain running maximum: the reference follows every new maximum
+            float m4[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                m4[i] = fmaxf(fmaxf(fmaxf(s[0][i], s[0][i + 4]), fmaxf(s[0][i + 8], s[0][i + 12])),
+                              fmaxf(fmaxf(s[1][i], s[1][i + 4]), fmaxf(s[1][i + 8], s[1][i + 12])));
+            const float mx = pair_max(fmaxf(fmaxf(m4[0], m4[1]), fmaxf(m4[2], m4[3]))) * c2;
+            const bool need = mx > rs.m;
+            if (__ballot(need)) move_reference(rs, need ? mx : rs.m);
+        }
         float part = exps(with_loads);
-        if (__ballot(!(part <= kSlackSum) || part > kSignificance * rs.l)) {
+        if (!early && __ballot(!(part <= kSlackSum) || part > kSignificance * rs.l)) {
             // row max as a tree (5 dependent levels)
             float v[32];
 #pragma unroll

@@ -192,7 +192,7 @@ __global__ __launch_bounds__(RTHREADS) void attn_rows_kernel(const AttnParams p)
     // reference m first, the row maximum only when some lane's weights sum
     // above 2^kRescaleSlack or above kSignificance of the running sum (the
     // first stage always, on flat rows the next few).
-    auto stage_step = [&](const unsigned char *ks_, const unsigned char *vs_, bool mask, int lim) {
+    auto stage_step = [&](const unsigned char *ks_, const unsigned char *vs_, bool mask, int lim, bool early) {
         u32x4 kf[D / 16], vf[8];
 #pragma unroll
         for (int ks = 0; ks < D / 16; ++ks) kf[ks] = *(const u32x4 *)(ks_ + ka[ks]);
@@ -235,8 +235,18 @@ __global__ __launch_bounds__(RTHREADS) void attn_rows_kernel(const AttnParams p)
             }
             return ls[0] + ls[1];
         };
+        if (early) {
+            // a plain running maximum on the first stages of the range
+            float mx = fmaxf(fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3])),
+                             fmaxf(fmaxf(sv[4], sv[5]), fmaxf(sv[6], sv[7])));
+            mx = fmaxf(mx, fmaxf(fmaxf(fmaxf(sv[8], sv[9]), fmaxf(sv[10], sv[11])),
+                                 fmaxf(fmaxf(sv[12], sv[13]), fmaxf(sv[14], sv[15]))));
+            mx = pair_max(mx) * c2;
+            const bool need = mx > rs.m;
+            if (__ballot(need)) move_reference(rs, need ? mx : rs.m);
+        }
         float part = exps();
-        if (__ballot(!(part <= kSlackSum) || part > kSignificance * rs.l)) {
+        if (!early && __ballot(!(part <= kSlackSum) || part > kSignificance * rs.l)) {
             float mx = sv[0];
 #pragma unroll
             for (int i = 1; i < 16; ++i) mx = fmaxf(mx, sv[i]);
@@ -277,7 +287,7 @@ __global__ __launch_bounds__(RTHREADS) void attn_rows_kernel(const AttnParams p)
             const bool mask = key0 + SKEYS > cache_end;
             const int64_t vis = min(pos, ke - 1) - key0;
             const int lim = (int)max((int64_t)-1, min(vis, (int64_t)SKEYS));
-            stage_step(ks_, vs_, mask, lim);
+            stage_step(ks_, vs_, mask, lim, u < kExactTiles);
         }
     }
 
