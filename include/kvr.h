@@ -23,7 +23,9 @@
  * Conventions shared by every entry point
  *   - Tensor pointers are DEVICE pointers owned by the caller; the library
  *     never allocates, frees or retains device memory and keeps no state
- *     between calls (every call is thread-safe).
+ *     between calls (every call is thread-safe) -- except
+ *     kvr_continue_noalloc, which keeps its split partials in a fixed buffer
+ *     inside the library (see there).
  *   - Layouts are dense row-major:
  *         Q, out            [tokens][n_q_heads][head_dim]
  *         K, V (new rows)   [tokens][n_kv_heads][head_dim]
@@ -51,7 +53,7 @@
 extern "C" {
 #endif
 
-#define KVR_ABI_VERSION 3
+#define KVR_ABI_VERSION 4
 
 typedef enum {
     KVR_OK = 0,
@@ -64,8 +66,10 @@ typedef enum {
     KVR_ERR_DEVICE = 7,    /* a HIP call or kernel launch failed                   */
     KVR_ERR_MISMATCH = 8,  /* an artifact's metadata does not match (model, dtype,
                               heads, head_dim, layers) or its header is not valid  */
-    KVR_ERR_POSITION = 9   /* a RoPE table without an entry for a position the call
+    KVR_ERR_POSITION = 9,  /* a RoPE table without an entry for a position the call
                               rotates, or invalid table arguments                  */
+    KVR_ERR_TOO_LARGE = 10 /* the call needs more scratch memory than the fixed
+                              buffer of kvr_continue_noalloc holds                 */
 } kvr_status;
 
 typedef enum { KVR_BF16 = 0, KVR_F32 = 1, KVR_F16 = 2 } kvr_dtype;
@@ -114,6 +118,27 @@ int kvr_prefill(const kvr_desc *desc, const void *Q, const void *K, const void *
 int kvr_continue(const kvr_desc *desc, const void *Qs, const void *Ks, const void *Vs,
                  const void *kcache, const void *vcache, int64_t L_prefix, int64_t S,
                  void *out, void *ws, size_t ws_bytes, void *stream);
+
+/*
+ * kvr_continue without a workspace argument, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc).  Arguments, layouts, results and errors are those of
+ * kvr_continue; the result is bit-identical to it.
+ *   The split partials go to a buffer of KVR_NOALLOC_SCRATCH_BYTES inside the
+ *   library, one per device, held from the first call on that device until the
+ *   process ends.  A call whose plan needs more (kvr_workspace_bytes(desc,
+ *   L_prefix, S, 1) > KVR_NOALLOC_SCRATCH_BYTES) returns KVR_ERR_TOO_LARGE and
+ *   launches nothing; every decode step and the 24-token continuation of a
+ *   32-query / 8-kv-head / 128-wide layer fit.  The call allocates nothing;
+ *   its first call on a device looks the buffer up (KVR_ERR_DEVICE if that
+ *   fails).  Every call on a device shares that device's buffer: calls that
+ *   may overlap on one device (different streams, threads) race and must be
+ *   ordered by the caller.  Nothing in the buffer needs clearing between calls.
+ */
+#define KVR_NOALLOC_SCRATCH_BYTES ((size_t)32 << 20)
+int kvr_continue_noalloc(const kvr_desc *desc, const void *Qs, const void *Ks, const void *Vs,
+                         const void *kcache, const void *vcache, int64_t L_prefix, int64_t S,
+                         void *out, void *stream);
 
 /*
  * Many independent continuations of one shared cached prefix (the paper's

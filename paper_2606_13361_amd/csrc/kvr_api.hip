@@ -5,6 +5,8 @@
 #include <math.h>
 #include <string.h>
 
+#include <mutex>
+
 #include "kvr.h"
 #include "kvr_internal.hpp"
 
@@ -337,6 +339,67 @@ int batched_impl(const kvr_desc *desc, const void *Qs, const void *Ks, const voi
     return KVR_OK;
 }
 
+// Host and device checks shared by kvr_continue and kvr_continue_noalloc
+// (everything but the workspace).
+int check_continue(const kvr_desc *desc, const void *Qs, const void *Ks, const void *Vs, const void *kcache,
+                   const void *vcache, int64_t L_prefix, int64_t S, void *out) {
+    int st = check_desc(desc);
+    if (st) return st;
+    if (L_prefix < 0 || S < 0 || S > kMaxTokens || L_prefix > kMaxKeys) return KVR_ERR_SHAPE;
+    if (L_prefix > desc->capacity) return KVR_ERR_CAPACITY;
+    if (S == 0) return KVR_OK;
+    if (!Qs || !Ks || !Vs || !out) return KVR_ERR_NULL;
+    if (L_prefix > 0 && (!kcache || !vcache)) return KVR_ERR_NULL;
+    if (!aligned16(Qs) || !aligned16(Ks) || !aligned16(Vs) || !aligned16(out) || !aligned16(kcache) ||
+        !aligned16(vcache))
+        return KVR_ERR_ALIGN;
+    return KVR_OK;
+}
+
+}  // namespace
+}  // namespace kvr
+
+// The split partials of kvr_continue_noalloc: a fixed buffer, one copy per
+// device, held until the process ends.  Host code uses the device address
+// that hipGetSymbolAddress returns for the current device, never this name
+// (on the host it only stands in for the symbol).
+static __device__ __align__(256) unsigned char scratch[KVR_NOALLOC_SCRATCH_BYTES];
+
+namespace kvr {
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch[kMaxDevices];
+
+// Device address of `scratch` on device dev, looked up once per device with
+// that device current (the caller's current device is restored).
+int scratch_on(int dev, void **ptr) {
+    if (dev < 0 || dev >= kMaxDevices) return KVR_ERR_DEVICE;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch[dev]) {
+        int cur = -1;
+        if (hipGetDevice(&cur) != hipSuccess) return KVR_ERR_DEVICE;
+        if (cur != dev && hipSetDevice(dev) != hipSuccess) return KVR_ERR_DEVICE;
+        void *p = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (cur != dev && hipSetDevice(cur) != hipSuccess) return KVR_ERR_DEVICE;
+        if (e != hipSuccess || !p) return KVR_ERR_DEVICE;
+        g_scratch[dev] = p;
+    }
+    *ptr = g_scratch[dev];
+    return KVR_OK;
+}
+
+// the device a stream belongs to (the current device for the null stream)
+int stream_device(hipStream_t stream, int *dev) {
+    if (!stream) return hipGetDevice(dev) == hipSuccess ? KVR_OK : KVR_ERR_DEVICE;
+    hipDevice_t d;
+    if (hipStreamGetDevice(stream, &d) != hipSuccess) return KVR_ERR_DEVICE;
+    *dev = (int)d;
+    return KVR_OK;
+}
+
 }  // namespace
 }  // namespace kvr
 
@@ -358,6 +421,7 @@ const char *kvr_strerror(int status) {
         case KVR_ERR_DEVICE: return "HIP call or kernel launch failed";
         case KVR_ERR_MISMATCH: return "artifact metadata does not match the running model (model id, dtype or shape)";
         case KVR_ERR_POSITION: return "RoPE table lacks a position the call rotates, or invalid table arguments";
+        case KVR_ERR_TOO_LARGE: return "the call needs more than the no-allocation entry point's fixed scratch buffer";
         default: return "unknown kvr status";
     }
 }
@@ -387,19 +451,31 @@ int kvr_prefill(const kvr_desc *desc, const void *Q, const void *K, const void *
 int kvr_continue(const kvr_desc *desc, const void *Qs, const void *Ks, const void *Vs, const void *kcache,
                  const void *vcache, int64_t L_prefix, int64_t S, void *out, void *ws, size_t ws_bytes,
                  void *stream) {
-    int st = check_desc(desc);
-    if (st) return st;
-    if (L_prefix < 0 || S < 0 || S > kMaxTokens || L_prefix > kMaxKeys) return KVR_ERR_SHAPE;
-    if (L_prefix > desc->capacity) return KVR_ERR_CAPACITY;
-    if (S == 0) return KVR_OK;
-    if (!Qs || !Ks || !Vs || !out) return KVR_ERR_NULL;
-    if (L_prefix > 0 && (!kcache || !vcache)) return KVR_ERR_NULL;
+    int st = check_continue(desc, Qs, Ks, Vs, kcache, vcache, L_prefix, S, out);
+    if (st || S == 0) return st;
     const Split sp = plan_split(desc, L_prefix, S);
     if (ws_bytes < sp.ws_bytes) return KVR_ERR_WORKSPACE;
     if (sp.ws_bytes > 0 && !ws) return KVR_ERR_NULL;
-    if (!aligned16(Qs) || !aligned16(Ks) || !aligned16(Vs) || !aligned16(out) || !aligned16(kcache) ||
-        !aligned16(vcache) || !aligned16(ws))
-        return KVR_ERR_ALIGN;
+    if (!aligned16(ws)) return KVR_ERR_ALIGN;
+    return launch_single(desc, kModeContinue, Qs, Ks, Vs, (void *)kcache, (void *)vcache, L_prefix, S, out,
+                         sp, ws, (hipStream_t)stream);
+}
+
+int kvr_continue_noalloc(const kvr_desc *desc, const void *Qs, const void *Ks, const void *Vs,
+                         const void *kcache, const void *vcache, int64_t L_prefix, int64_t S, void *out,
+                         void *stream) {
+    int st = check_continue(desc, Qs, Ks, Vs, kcache, vcache, L_prefix, S, out);
+    if (st || S == 0) return st;
+    const Split sp = plan_split(desc, L_prefix, S);
+    if (sp.ws_bytes > KVR_NOALLOC_SCRATCH_BYTES) return KVR_ERR_TOO_LARGE;
+    void *ws = nullptr;
+    if (sp.ws_bytes > 0) {
+        int dev = -1;
+        st = stream_device((hipStream_t)stream, &dev);
+        if (st) return st;
+        st = scratch_on(dev, &ws);
+        if (st) return st;
+    }
     return launch_single(desc, kModeContinue, Qs, Ks, Vs, (void *)kcache, (void *)vcache, L_prefix, S, out,
                          sp, ws, (hipStream_t)stream);
 }

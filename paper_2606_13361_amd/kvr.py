@@ -17,11 +17,13 @@ LIB_PATH = os.path.join(_PKG, "libkvr.so")
 
 KVR_OK, KVR_ERR_NULL, KVR_ERR_SHAPE, KVR_ERR_DTYPE = 0, 1, 2, 3
 KVR_ERR_CAPACITY, KVR_ERR_WORKSPACE, KVR_ERR_ALIGN, KVR_ERR_DEVICE = 4, 5, 6, 7
-KVR_ERR_MISMATCH, KVR_ERR_POSITION = 8, 9
+KVR_ERR_MISMATCH, KVR_ERR_POSITION, KVR_ERR_TOO_LARGE = 8, 9, 10
+KVR_NOALLOC_SCRATCH_BYTES = 32 << 20
 KVR_ARTIFACT_HEADER_BYTES = 256
 KVR_BF16, KVR_F32, KVR_F16 = 0, 1, 2
 
-EXPORTS = ("kvr_prefill", "kvr_continue", "kvr_continue_append", "kvr_continue_batched", "kvr_cache_append",
+EXPORTS = ("kvr_prefill", "kvr_continue", "kvr_continue_append", "kvr_continue_noalloc", "kvr_continue_batched",
+           "kvr_cache_append",
            "kvr_workspace_bytes", "kvr_strerror", "kvr_abi_version",
            "kvr_q8_bytes", "kvr_quantize_cache", "kvr_continue_q8",
            "kvr_artifact_bytes", "kvr_artifact_save", "kvr_artifact_load",
@@ -65,6 +67,7 @@ def load():
     lib.kvr_prefill.argtypes = [D, P, P, P, I64, P, P, P, P]
     lib.kvr_continue.argtypes = [D, P, P, P, P, P, I64, I64, P, P, SZ, P]
     lib.kvr_continue_append.argtypes = [D, P, P, P, P, P, I64, I64, P, P, SZ, P]
+    lib.kvr_continue_noalloc.argtypes = [D, P, P, P, P, P, I64, I64, P, P]
     lib.kvr_continue_batched.argtypes = [D, P, P, P, ctypes.POINTER(ctypes.c_int32), ctypes.c_int32,
                                          P, P, I64, P, P, SZ, P]
     lib.kvr_cache_append.argtypes = [D, P, P, I64, P, P, I64, P]
@@ -92,7 +95,8 @@ def load():
     lib.kvr_strerror.argtypes = [ctypes.c_int]
     lib.kvr_strerror.restype = ctypes.c_char_p
     lib.kvr_abi_version.argtypes = []
-    for f in (lib.kvr_prefill, lib.kvr_continue, lib.kvr_continue_append, lib.kvr_continue_batched,
+    for f in (lib.kvr_prefill, lib.kvr_continue, lib.kvr_continue_append, lib.kvr_continue_noalloc,
+              lib.kvr_continue_batched,
               lib.kvr_cache_append,
               lib.kvr_abi_version, lib.kvr_quantize_cache, lib.kvr_continue_q8, lib.kvr_artifact_save,
               lib.kvr_artifact_load, lib.kvr_rope_table, lib.kvr_rope_apply, lib.kvr_prefill_rope,
@@ -178,6 +182,18 @@ def kvr_continue(desc, Qs, Ks, Vs, kcache, vcache, L_prefix, S, out, ws=None, st
     wp, wn = _workspace(ws)
     _raise(load().kvr_continue(ctypes.byref(desc), q, k, v, kc, vc, int(L_prefix), int(S), o, wp, wn,
                                _stream(stream)), "kvr_continue")
+
+
+def kvr_continue_noalloc(desc, Qs, Ks, Vs, kcache, vcache, L_prefix, S, out, stream=None):
+    """kvr_continue with its split partials in the library's fixed per-device buffer."""
+    Hq, Hkv, d = desc.n_q_heads, desc.n_kv_heads, desc.head_dim
+    q = _check(Qs, "Qs", desc, (S, Hq, d))
+    k = _check(Ks, "Ks", desc, (S, Hkv, d))
+    v = _check(Vs, "Vs", desc, (S, Hkv, d))
+    o = _check(out, "out", desc, (S, Hq, d))
+    kc, vc = _cache_ptrs(desc, kcache, vcache, L_prefix > 0)
+    _raise(load().kvr_continue_noalloc(ctypes.byref(desc), q, k, v, kc, vc, int(L_prefix), int(S), o,
+                                       _stream(stream)), "kvr_continue_noalloc")
 
 
 def kvr_continue_append(desc, Qs, Ks, Vs, kcache, vcache, L_prefix, S, out, ws=None, stream=None):

@@ -70,8 +70,8 @@ def test_exports_match_header(lib):
 
 
 def test_abi_version_and_strerror(lib):
-    assert lib.kvr_abi_version() == 3
-    for code in range(10):
+    assert lib.kvr_abi_version() == 4
+    for code in range(11):
         assert len(lib.kvr_strerror(code)) > 0
     assert b"unknown" in lib.kvr_strerror(99)
 
@@ -273,3 +273,27 @@ def test_continue_append_errors(lib):
     for kw in ("Q", "K", "V", "out", "kc", "vc"):
         assert f(**{kw: None}) == kvr.KVR_ERR_NULL, kw    # the caches are written: always needed
         assert f(**{kw: MIS}) == kvr.KVR_ERR_ALIGN, kw
+
+
+def noalloc(lib, d, Lp=64, S=8, Q=A, K=A, V=A, kc=A, vc=A, out=A):
+    return lib.kvr_continue_noalloc(ctypes.byref(d), Q, K, V, kc, vc, Lp, S, out, None)
+
+
+def test_noalloc_rejections(lib):
+    """kvr_continue_noalloc: kvr_continue's argument checks, and a plan whose split
+    partials exceed the fixed buffer is KVR_ERR_TOO_LARGE -- all before any HIP call."""
+    d = desc(capacity=1 << 20)
+    assert noalloc(lib, desc(n_q_heads=30)) == kvr.KVR_ERR_SHAPE
+    assert noalloc(lib, desc(dtype=7)) == kvr.KVR_ERR_DTYPE
+    assert noalloc(lib, d, Lp=-1) == kvr.KVR_ERR_SHAPE
+    assert noalloc(lib, desc(capacity=100), Lp=101) == kvr.KVR_ERR_CAPACITY
+    assert noalloc(lib, d, Q=None) == kvr.KVR_ERR_NULL
+    assert noalloc(lib, d, kc=None) == kvr.KVR_ERR_NULL
+    assert noalloc(lib, d, out=MIS) == kvr.KVR_ERR_ALIGN
+    assert noalloc(lib, d, S=0, Q=None, K=None, V=None, out=None) == kvr.KVR_OK
+    Lp, S = 20000, 256
+    assert lib.kvr_workspace_bytes(ctypes.byref(d), Lp, S, 1) > kvr.KVR_NOALLOC_SCRATCH_BYTES
+    assert noalloc(lib, d, Lp=Lp, S=S) == kvr.KVR_ERR_TOO_LARGE
+    # the Qwen-shaped 24-token continuation and every decode step fit
+    for Lp, S in ((32768, 24), (32768, 1), (1 << 19, 1), (3774, 24)):
+        assert lib.kvr_workspace_bytes(ctypes.byref(d), Lp, S, 1) <= kvr.KVR_NOALLOC_SCRATCH_BYTES
