@@ -2,19 +2,24 @@
 """Benchmark of the prefill / prefix-reuse attention path on one MI355X.
 
 One step = one pass of the whole hot path over a Qwen3-4B-shaped attention
-layer (32 query heads, 8 kv heads, head_dim 128, bf16, synthetic N(0,1)):
-  1. kvr_prefill           3798 tokens (attention + cache fill)
-  2. kvr_continue          24 tokens over the cached 3774
-  3. kvr_cache_append      their 24 K/V rows
-  4. kvr_continue_batched  64 readers of the same cached 3774-token prefix,
-                           suffix lengths U[24, 256]
-  5. decode step           kvr_continue(S=1) over 3798 + kvr_cache_append
-Every call is timed with HIP events on the stream it runs on.
+layer (32 query heads, 8 kv heads, head_dim 128, bf16, synthetic N(0,1)) at
+the long context the targets are stated for:
+  1. kvr_prefill           32792 tokens (attention + cache fill)      <- `value`
+  2. kvr_continue          24 tokens over a cached 32768-token prefix
+  3. kvr_continue          24 tokens over a cached 16384-token prefix
+  4. kvr_cache_append      the 24 new K/V rows after the 32768-token prefix
+  5. kvr_continue_batched  64 readers (S ~ U[24, 256]) of one cached
+                           3774-token prefix
+  6. decode step           kvr_continue_append(S=1) over 32768 cached rows
+Every call is timed with HIP events on the stream it runs on.  The
+continuations read caches from pools of >= 1 GiB (each step reads a cache
+last touched several steps earlier), so the 256 MB last-level cache cannot
+serve them.
 
 After the timed steps, the length sweep (prefix 1024 / 4096 / 16384 / 32768,
-S = 24) and the 36-layer decode chain (32768-token caches, 24 steps of S=1)
-are measured; continuation timings rotate over >= 1 GiB of distinct caches so
-that the 256 MB last-level cache cannot serve them.
+S = 24, continuations graph-replayed over rotated caches), the 36-layer
+decode chain (32768-token caches, 24 steps of S=1) and a CPU-oracle baseline
+on a bounded sample of the 32792-token prefill are measured.
 
 Prints ONE JSON line.
 """
@@ -80,8 +85,6 @@ def main():
     stream = torch.cuda.current_stream()
     sh = W.QWEN
     Hq, Hkv, D = sh.n_q_heads, sh.n_kv_heads, sh.head_dim
-    L, S = W.LAYER_L, W.LAYER_S
-    n = L + S
 
     if args.copy_calibration:
         # a plain copy of known size: reads 1 GiB, writes 1 GiB
@@ -92,42 +95,64 @@ def main():
         del a, b
 
     # ---------------------------------------------------------------- inputs
-    q, k, v = W.qkv(n, sh, seed=0)
-    qd, kd, vd = q.to(dev), k.to(dev), v.to(dev)
-    cap = n + 1
-    desc = kvr.make_desc(Hq, Hkv, D, torch.bfloat16, cap)
-    kc = torch.zeros((Hkv, cap, D), dtype=torch.bfloat16, device=dev)
-    vc = torch.zeros_like(kc)
-    out_full = torch.empty_like(qd)
-    qs, ks, vs = qd[L:].contiguous(), kd[L:].contiguous(), vd[L:].contiguous()
-    out_c = torch.empty_like(qs)
-    ws = kvr.workspace_for(desc, L, S)
+    L32, L16, S = W.SWEEP_L[3], W.SWEEP_L[2], W.SWEEP_S
+    n32, n16 = L32 + S, L16 + S
+    q, k, v = W.qkv_device(n32, sh, seed=L32, device=dev)
+    desc32 = kvr.make_desc(Hq, Hkv, D, torch.bfloat16, n32 + 1)
+    desc16 = kvr.make_desc(Hq, Hkv, D, torch.bfloat16, n16 + 1)
+    out_full = torch.empty_like(q)
+    qs, ks, vs = q[L32:].contiguous(), k[L32:].contiguous(), v[L32:].contiguous()
+    out_c32, out_c16 = torch.empty_like(qs), torch.empty_like(qs)
+    ws32, ws16 = kvr.workspace_for(desc32, L32, S), kvr.workspace_for(desc16, L16, S)
+    # cache pools of >= 1 GiB each: the prefill of step i fills pool32[i % R32];
+    # the continuations of step i read caches last written R32 / 2 (R16) steps before
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(5)
+
+    def pool(n_rows):
+        cache_bytes = 2 * Hkv * n_rows * D * ELT
+        R = max(2, -(-(1 << 30) // cache_bytes))
+        pl = torch.empty((R, 2, Hkv, n_rows, D), dtype=torch.bfloat16, device=dev)
+        for i in range(R):
+            pl[i].copy_(torch.randn((2, Hkv, n_rows, D), generator=gen, device=dev))
+        return pl, R
+    pool32, R32 = pool(n32 + 1)
+    pool16, R16 = pool(n16 + 1)
+    # many readers of one 3774-token prefix
+    Lr = W.READERS_L
+    desc_r = kvr.make_desc(Hq, Hkv, D, torch.bfloat16, Lr)
+    kc_r = torch.randn((Hkv, Lr, D), generator=gen, device=dev).to(torch.bfloat16)
+    vc_r = torch.randn((Hkv, Lr, D), generator=gen, device=dev).to(torch.bfloat16)
     lens = W.reader_lengths()
     cu = W.cu_seqlens(lens)
-    rq, rk, rv = W.qkv(cu[-1], sh, seed=1)
-    rq, rk, rv = rq.to(dev), rk.to(dev), rv.to(dev)
+    rq, rk, rv = W.qkv_device(cu[-1], sh, seed=1, device=dev)
     rout = torch.empty_like(rq)
-    dq, dk, dv = (x.to(dev) for x in W.qkv(1, sh, seed=2))
+    dq, dk, dv = W.qkv_device(1, sh, seed=2, device=dev)
     dout = torch.empty_like(dq)
-    ws_dec = kvr.workspace_for(desc, n, 1)
+    ws_dec = kvr.workspace_for(desc32, L32, 1)
 
-    names = ["prefill", "continue", "append", "readers", "decode_step"]
+    names = ["prefill", "continue32k", "continue16k", "append", "readers", "decode_step"]
 
-    def step(ev=None):
-        def rec(i):
+    def step(i, ev=None):
+        def rec(j):
             if ev is not None:
-                ev[i].record(stream)
+                ev[j].record(stream)
+        c_new = pool32[i % R32]
+        c_old = pool32[(i + R32 // 2) % R32]
+        c16 = pool16[i % R16]
         rec(0)
-        kvr.kvr_prefill(desc, qd, kd, vd, n, out_full, kc, vc)
+        kvr.kvr_prefill(desc32, q, k, v, n32, out_full, c_new[0], c_new[1])
         rec(1)
-        kvr.kvr_continue(desc, qs, ks, vs, kc, vc, L, S, out_c, ws)
+        kvr.kvr_continue(desc32, qs, ks, vs, c_old[0], c_old[1], L32, S, out_c32, ws32)
         rec(2)
-        kvr.kvr_cache_append(desc, ks, vs, S, kc, vc, L)
+        kvr.kvr_continue(desc16, qs, ks, vs, c16[0], c16[1], L16, S, out_c16, ws16)
         rec(3)
-        kvr.kvr_continue_batched(desc, rq, rk, rv, cu, kc, vc, L, rout)
+        kvr.kvr_cache_append(desc32, ks, vs, S, c_new[0], c_new[1], L32)
         rec(4)
-        kvr.kvr_continue_append(desc, dq, dk, dv, kc, vc, n, 1, dout, ws_dec)
+        kvr.kvr_continue_batched(desc_r, rq, rk, rv, cu, kc_r, vc_r, Lr, rout)
         rec(5)
+        kvr.kvr_continue_append(desc32, dq, dk, dv, c_old[0], c_old[1], L32, 1, dout, ws_dec)
+        rec(6)
 
     if args.model_only:
         print(json.dumps({"model": model_table1(torch, A, W, dev)}), flush=True)
@@ -140,14 +165,14 @@ def main():
         print(json.dumps(res), flush=True)
         return
 
-    for _ in range(args.warmup):
-        step()
+    for i in range(args.warmup):
+        step(i)
     torch.cuda.synchronize()
     events = [[torch.cuda.Event(enable_timing=True) for _ in range(len(names) + 1)] for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
-        step(events[i])
+        step(args.warmup + i, events[i])
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     per = {nm: [] for nm in names}
@@ -157,16 +182,22 @@ def main():
     avg = {nm: sum(v_) / len(v_) for nm, v_ in per.items()}
     med = {nm: sorted(v_)[len(v_) // 2] for nm, v_ in per.items()}
 
-    pf_flops = A.prefill_flops(n, Hq, D)
+    pf_flops = A.prefill_flops(n32, Hq, D)
     pf_tflops = pf_flops / avg["prefill"] / 1e12
-    c_bytes = A.continue_bytes(L, S, Hq, Hkv, D, ELT)
-    c_gbps = c_bytes / avg["continue"] / 1e9
-    rd_flops = A.batched_flops(L, lens, Hq, D)
+    c32_bytes = A.continue_bytes(L32, S, Hq, Hkv, D, ELT)
+    c16_bytes = A.continue_bytes(L16, S, Hq, Hkv, D, ELT)
+    c32_gbps = c32_bytes / avg["continue32k"] / 1e9
+    c16_gbps = c16_bytes / avg["continue16k"] / 1e9
+    rd_flops = A.batched_flops(Lr, lens, Hq, D)
     rd_tflops = rd_flops / avg["readers"] / 1e12
-    dec_bytes = A.continue_bytes(n, 1, Hq, Hkv, D, ELT) + A.append_bytes(1, Hkv, D, ELT)
+    dec_bytes = A.continue_bytes(L32, 1, Hq, Hkv, D, ELT) + A.append_bytes(1, Hkv, D, ELT)
 
-    # parity spot check of this very run (continuation vs prefill rows, Claim 1)
-    claim1 = float((out_c - out_full[L:]).abs().max())
+    # parity spot check of this very run (Claim 1): the continuation over the
+    # cache the last prefill wrote, against that prefill's rows
+    last = pool32[(args.warmup + args.steps - 1) % R32]
+    kvr.kvr_continue(desc32, qs, ks, vs, last[0], last[1], L32, S, out_c32, ws32)
+    torch.cuda.synchronize()
+    claim1 = float((out_c32 - out_full[L32:]).abs().max())
 
     result = {
         "metric": METRIC,
@@ -183,54 +214,63 @@ def main():
         "data": "synthetic: Q/K/V ~ N(0,1), seeded (no document text or weights)",
         "config": {
             "workload": "Qwen3-4B-shaped attention layer, 32 q heads / 8 kv heads / head_dim 128, bf16, "
-                        "batch 1: prefill 3798 tokens; continue 24 tokens over the cached 3774; 64 readers "
-                        "(S ~ U[24,256]) over the same cache; one decode step",
-            "prefix_tokens": L, "suffix_tokens": S, "readers": len(lens), "reader_tokens": cu[-1],
-            "global_batch": 1, "seq_len": n,
+                        "batch 1: prefill 32792 tokens (value); continue 24 tokens over cached 32768- and "
+                        "16384-token prefixes; 64 readers (S ~ U[24,256]) of a cached 3774-token prefix; "
+                        "one decode step over 32768",
+            "prefill_tokens": n32, "prefix_tokens": [L32, L16], "suffix_tokens": S,
+            "readers": len(lens), "reader_prefix": Lr, "reader_tokens": cu[-1],
+            "global_batch": 1, "seq_len": n32,
         },
         "prefill_ms": round(avg["prefill"] * 1e3, 4),
         "prefill_tflops": round(pf_tflops, 2),
         "prefill_mfma_frac": round(pf_tflops / PEAK_BF16_TFLOPS, 4),
-        "continue_us": round(avg["continue"] * 1e6, 2),
-        "continue_GBps": round(c_gbps, 1),
-        "continue_hbm_frac": round(c_gbps / PEAK_HBM_GBPS, 4),
-        "continue_note": "15.5 MB cache: served from the 256 MB last-level cache, launch-bound; "
-                         "see sweep for the HBM-bound lengths",
-        "reuse_speedup": round(avg["prefill"] / avg["continue"], 2),
-        "break_even_N": round(A.break_even(avg["prefill"], avg["continue"]), 4),
+        "continue32k_us": round(avg["continue32k"] * 1e6, 2),
+        "continue32k_GBps": round(c32_gbps, 1),
+        "continue32k_hbm_frac": round(c32_gbps / PEAK_HBM_GBPS, 4),
+        "continue16k_us": round(avg["continue16k"] * 1e6, 2),
+        "continue16k_GBps": round(c16_gbps, 1),
+        "continue16k_hbm_frac": round(c16_gbps / PEAK_HBM_GBPS, 4),
+        "continue_caches": "pools of %d x 32768- and %d x 16384-token caches (>= 1 GiB each), read "
+                           "several steps after they were last written" % (R32, R16),
+        "reuse_speedup_32k": round(avg["prefill"] / avg["continue32k"], 2),
+        "break_even_N_32k": round(A.break_even(avg["prefill"], avg["continue32k"]), 4),
         "append24_us": round(avg["append"] * 1e6, 2),
         "readers_ms": round(avg["readers"] * 1e3, 4),
         "readers_tflops": round(rd_tflops, 2),
         "readers_mfma_frac": round(rd_tflops / PEAK_BF16_TFLOPS, 4),
         "decode_step_us": round(avg["decode_step"] * 1e6, 2),
         "decode_step_GBps": round(dec_bytes / avg["decode_step"] / 1e9, 1),
+        "decode_step_hbm_frac": round(dec_bytes / avg["decode_step"] / 1e9 / PEAK_HBM_GBPS, 4),
         "median_ms": {nm: round(med[nm] * 1e3, 4) for nm in names},
         "claim1_maxabs": claim1,
         "paper_context": "paper Table 1: full-model reuse 8.6-49.7x cheaper (Qwen3-4B fp16, Apple M1 Pro "
                          "MPS, one continuation step); not comparable hardware or scope",
     }
-    # rooflines of the step's kernels; `roofline` is the one that takes the most time
+    # rooflines of the step's calls; `roofline` is the one that takes the most time
     digest = kernel_source_digest()
     traffic = measured_traffic(digest)
+
+    def roof(call, kernel, bound, achieved, work, t):
+        peak = PEAK_BF16_TFLOPS if bound == "mfma" else PEAK_HBM_GBPS
+        return {"call": call, "kernel": kernel, "bound": bound, "achieved": round(achieved, 2), "peak": peak,
+                "unit": "TFLOP/s" if bound == "mfma" else "GB/s", "frac": round(achieved / peak, 4),
+                "work_per_launch": work, "avg_launch_ms": round(t * 1e3, 4), "traffic": traffic.get(call)}
     roofs = {
-        "readers": {"kernel": "attn_pp_kernel<readers>", "bound": "mfma", "achieved": round(rd_tflops, 2),
-                    "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(rd_tflops / PEAK_BF16_TFLOPS, 4),
-                    "work_per_launch": rd_flops, "avg_launch_ms": round(avg["readers"] * 1e3, 4)},
-        "prefill": {"kernel": "attn_pp_kernel<prefill>", "bound": "mfma", "achieved": round(pf_tflops, 2),
-                    "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(pf_tflops / PEAK_BF16_TFLOPS, 4),
-                    "work_per_launch": pf_flops, "avg_launch_ms": round(avg["prefill"] * 1e3, 4)},
-        "continue": {"kernel": "attn_rows_kernel + merge_bf16_kernel<128>", "bound": "hbm",
-                     "achieved": round(c_gbps, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
-                     "frac": round(c_gbps / PEAK_HBM_GBPS, 4), "work_per_launch": c_bytes,
-                     "avg_launch_ms": round(avg["continue"] * 1e3, 4)},
+        "prefill": roof("prefill", "attn_pp_kernel<prefill>", "mfma", pf_tflops, pf_flops, avg["prefill"]),
+        "continue32k": roof("continue32k", "attn_cont_kernel<3> + merge_bf16_kernel<128>", "hbm", c32_gbps,
+                            c32_bytes, avg["continue32k"]),
+        "continue16k": roof("continue16k", "attn_rows_kernel + merge_bf16_kernel<128>", "hbm", c16_gbps,
+                            c16_bytes, avg["continue16k"]),
+        "readers": roof("readers", "attn_pp_kernel<readers>", "mfma", rd_tflops, rd_flops, avg["readers"]),
+        "decode_step": roof("decode_step", "attn_cont_kernel<1> + merge_bf16_kernel<128>", "hbm",
+                            dec_bytes / avg["decode_step"] / 1e9, dec_bytes, avg["decode_step"]),
     }
-    for r in roofs.values():
-        t = traffic.get(r["kernel"])
-        r["traffic"] = t
-    dominant = max(roofs, key=lambda k: roofs[k]["avg_launch_ms"])
-    result["roofline"] = dict(roofs[dominant], call=dominant)
+    dominant = max(roofs, key=lambda c: roofs[c]["avg_launch_ms"])
+    result["roofline"] = roofs[dominant]
     result["rooflines"] = roofs
     result["kernel_source_digest"] = digest
+    del pool32, pool16, q, k, v, out_full
+    torch.cuda.empty_cache()
 
     if not args.no_sweep:
         lens_ = [int(x) for x in args.sweep_lengths.split(",")] if args.sweep_lengths else list(W.SWEEP_L)
@@ -244,7 +284,7 @@ def main():
     if not args.no_model:
         result["model"] = model_table1(torch, A, W, dev)
     if not args.no_cpu_baseline:
-        result["cpu_baseline"] = cpu_baseline(q, k, v, A, args.cpu_seconds)
+        result["cpu_baseline"] = cpu_baseline(W, A, args.cpu_seconds)
     print(json.dumps(result), flush=True)
 
 
@@ -680,38 +720,80 @@ def model_table1(torch, A, W, dev, lengths=(255, 485, 945, 1888, 3774)):
     return res
 
 
-def cpu_baseline(q, k, v, A, target_s):
-    """The fp64 oracle on a strided sample of the prefill rows, on the host cores."""
-    from oracle import ref
+def host_cpu():
+    """The host's logical CPUs, the ones this process may run on, the cgroup CPU
+    quota (if any) and the CPU model."""
+    info = {"host_logical_cpus": os.cpu_count()}
     try:
-        cores = len(os.sched_getaffinity(0))
+        info["affinity_cpus"] = len(os.sched_getaffinity(0))
     except AttributeError:
-        cores = os.cpu_count() or 1
-    cores = max(1, min(cores, 16))
-    n, Hq, D = q.shape
+        info["affinity_cpus"] = os.cpu_count()
+    try:
+        quota, period = open("/sys/fs/cgroup/cpu.max").read().split()[:2]
+        info["cgroup_cpu_quota"] = None if quota == "max" else round(int(quota) / int(period), 2)
+    except (OSError, ValueError):
+        info["cgroup_cpu_quota"] = None
+    model = None
+    try:
+        for ln in open("/proc/cpuinfo"):
+            if ln.startswith("model name"):
+                model = ln.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    info["cpu_model"] = model
+    return info
+
+
+def cpu_baseline(W, A, target_s):
+    """The fp64 oracle, as it stands, on a strided sample of the rows of the
+    32792-token prefill (the `value` workload), timed on the host cores: every
+    CPU of the affinity mask (median of 3 runs) and one thread (median of 3, on
+    a smaller sample).  Inputs are the same seeded bf16 values, drawn on the
+    CPU, widened to fp64 once before timing."""
+    import numpy as np
+    from oracle import ref
+    host = host_cpu()
+    threads = max(1, host["affinity_cpus"] or 1)
+    sh = W.QWEN
+    n = W.SWEEP_L[3] + W.SWEEP_S
+    Hq, D = sh.n_q_heads, sh.head_dim
+    q, k, v = W.qkv(n, sh, seed=0)
+    q, k, v = (ref._f64(x) for x in (q, k, v))
 
     def flops(rows):
         return sum(4 * Hq * D * (r + 1) for r in rows)
 
-    probe = list(range(n - 1, 0, -n // 8))[:8]
-    t0 = time.perf_counter()
-    ref.prefill(q, k, v, rows=probe, nthreads=cores)
-    dt = max(time.perf_counter() - t0, 1e-3)
-    rate = flops(probe) / dt
-    want_flops = rate * target_s
-    total = A.prefill_flops(n, Hq, D)
-    step = max(1, int(total / max(want_flops, 1.0)))
-    rows = list(range(step // 2, n, step))
-    t0 = time.perf_counter()
-    ref.prefill(q, k, v, rows=rows, nthreads=cores)
-    dt = time.perf_counter() - t0
+    def sample(rate, seconds):
+        step = max(1, int(A.prefill_flops(n, Hq, D) / max(rate * seconds, 1.0)))
+        return list(range(step // 2, n, step)), step
+
+    def run(rows, nth):
+        t0 = time.perf_counter()
+        ref.prefill(q, k, v, rows=rows, nthreads=nth)
+        return time.perf_counter() - t0
+
+    res = {}
+    for label, nth, secs in (("all", threads, target_s / 3.0), ("one", 1, target_s / 6.0)):
+        probe = list(range(n - 1, 0, -n // (min(2 * nth, 64) + 2)))[:min(2 * nth, 64)]
+        rate = flops(probe) / max(run(probe, nth), 1e-3)
+        rows, step = sample(rate, secs)
+        ts = sorted(run(rows, nth) for _ in range(3))
+        res[label] = (flops(rows) / ts[1] / 1e12, rows, step, ts)
+    v_all, rows, step, ts = res["all"]
+    v_one, rows1, step1, ts1 = res["one"]
     return {
-        "value": round(flops(rows) / dt / 1e12, 6),
+        "value": round(v_all, 6),
         "unit": "TFLOP/s",
-        "cores": cores,
+        "cores": threads,
         "kind": "oracle",
-        "sample": "fp64 oracle prefill rows %d..%d step %d (%d of %d rows, all 32 heads) of the "
-                  "3798-token layer, %.1f s" % (rows[0], rows[-1], step, len(rows), n, dt),
+        "sample": "fp64 oracle prefill rows %d..%d step %d (%d of %d rows, all 32 heads) of the 32792-token "
+                  "layer, median of 3 runs of %.1f-%.1f s on %d threads" % (rows[0], rows[-1], step, len(rows), n,
+                                                                             ts[0], ts[2], threads),
+        "single_thread_value": round(v_one, 6),
+        "single_thread_sample": "rows step %d (%d rows), median of 3 runs of %.1f-%.1f s" % (
+            step1, len(rows1), ts1[0], ts1[2]),
+        "host": host,
     }
 
 

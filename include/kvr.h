@@ -135,7 +135,7 @@ int kvr_continue(const kvr_desc *desc, const void *Qs, const void *Ks, const voi
  *   may overlap on one device (different streams, threads) race and must be
  *   ordered by the caller.  Nothing in the buffer needs clearing between calls.
  */
-#define KVR_NOALLOC_SCRATCH_BYTES ((size_t)32 << 20)
+#define KVR_NOALLOC_SCRATCH_BYTES ((size_t)16 << 20)
 int kvr_continue_noalloc(const kvr_desc *desc, const void *Qs, const void *Ks, const void *Vs,
                          const void *kcache, const void *vcache, int64_t L_prefix, int64_t S,
                          void *out, void *stream);

@@ -18,7 +18,7 @@ LIB_PATH = os.path.join(_PKG, "libkvr.so")
 KVR_OK, KVR_ERR_NULL, KVR_ERR_SHAPE, KVR_ERR_DTYPE = 0, 1, 2, 3
 KVR_ERR_CAPACITY, KVR_ERR_WORKSPACE, KVR_ERR_ALIGN, KVR_ERR_DEVICE = 4, 5, 6, 7
 KVR_ERR_MISMATCH, KVR_ERR_POSITION, KVR_ERR_TOO_LARGE = 8, 9, 10
-KVR_NOALLOC_SCRATCH_BYTES = 32 << 20
+KVR_NOALLOC_SCRATCH_BYTES = 16 << 20
 KVR_ARTIFACT_HEADER_BYTES = 256
 KVR_BF16, KVR_F32, KVR_F16 = 0, 1, 2
 
