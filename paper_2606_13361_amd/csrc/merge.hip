@@ -14,6 +14,8 @@
 // 16 loads in flight.  Block b serves kv head b % Hkv, the same residue the
 // attention kernel gives the head's blocks, so with 8 kv heads the partials
 // are read on the XCD whose L2 took them.
+#include <type_traits>
+
 #include "attn_common.hpp"
 
 namespace kvr {
@@ -22,7 +24,7 @@ namespace {
 using namespace dev;
 
 constexpr int MERGE_THREADS = 64;
-constexpr int MERGE_BATCH = 16;   // split loads in flight per lane
+constexpr int MERGE_BATCH = 16;   // split loads in flight per lane (more than 32 splits)
 
 template <int D, class E>
 __global__ __launch_bounds__(MERGE_THREADS) void merge_bf16_kernel(const MergeParams p) {
@@ -41,6 +43,54 @@ __global__ __launch_bounds__(MERGE_THREADS) void merge_bf16_kernel(const MergePa
     const int64_t row = (int64_t)g * p.rows + (valid ? r : r0);   // rows past the end read row r0
     const float *src = p.ws + row * D + 4 * part;
     const int64_t sstride = per_split * D;
+    auto store_row = [&](const float4 &acc, float l) {
+        const float il = l > 0.f ? 1.f / l : 0.f;
+        const int tok = r / p.group;
+        const int head = g * p.group + r % p.group;
+        uint16_t *out = (uint16_t *)p.out + ((int64_t)tok * p.n_q_heads + head) * D + 4 * part;
+        u32x2 v;
+        v[0] = E::pack2(acc.x * il, acc.y * il);
+        v[1] = E::pack2(acc.z * il, acc.w * il);
+        *(u32x2 *)out = v;
+    };
+
+    // up to 16 or 32 splits: every split's (m, l) and partial row at once, one
+    // memory round trip; each lane reads all of its row's records itself (the
+    // row's lanes read the same addresses), no LDS and no shuffles.  Indices
+    // past nsplit re-read the last split and get weight 0.
+    auto one_trip = [&](auto ns_tag) {
+        constexpr int NS = decltype(ns_tag)::value;
+        float4 o[NS];
+        float2 ml2[NS];
+#pragma unroll
+        for (int k = 0; k < NS; ++k) o[k] = *(const float4 *)(src + min(k, p.nsplit - 1) * sstride);
+#pragma unroll
+        for (int k = 0; k < NS; ++k) ml2[k] = *(const float2 *)(ml + (min(k, p.nsplit - 1) * per_split + row) * 2);
+        __builtin_amdgcn_sched_barrier(0);   // every load issued before any use
+        float M = -INFINITY;
+#pragma unroll
+        for (int k = 0; k < NS; ++k) M = fmaxf(M, ml2[k].x);
+        float l = 0.f;
+        float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+        for (int k = 0; k < NS; ++k) {
+            const float w = k < p.nsplit ? __builtin_amdgcn_exp2f(ml2[k].x - M) : 0.f;
+            l = __builtin_fmaf(w, ml2[k].y, l);
+            acc.x = __builtin_fmaf(w, o[k].x, acc.x);
+            acc.y = __builtin_fmaf(w, o[k].y, acc.y);
+            acc.z = __builtin_fmaf(w, o[k].z, acc.z);
+            acc.w = __builtin_fmaf(w, o[k].w, acc.w);
+        }
+        if (valid) store_row(acc, l);
+    };
+    if (p.nsplit <= 16) {
+        one_trip(std::integral_constant<int, 16>{});
+        return;
+    }
+    if (p.nsplit <= 32) {
+        one_trip(std::integral_constant<int, 32>{});
+        return;
+    }
 
     // the first MERGE_BATCH splits' partial rows do not depend on the
     // weights: their loads go out before the (m, l) round trip (split indices
@@ -99,14 +149,7 @@ __global__ __launch_bounds__(MERGE_THREADS) void merge_bf16_kernel(const MergePa
         acc.z = __builtin_fmaf(w, o.z, acc.z);
         acc.w = __builtin_fmaf(w, o.w, acc.w);
     }
-    const float il = l > 0.f ? 1.f / l : 0.f;
-    const int tok = r / p.group;
-    const int head = g * p.group + r % p.group;
-    uint16_t *out = (uint16_t *)p.out + ((int64_t)tok * p.n_q_heads + head) * D + 4 * part;
-    u32x2 v;
-    v[0] = E::pack2(acc.x * il, acc.y * il);
-    v[1] = E::pack2(acc.z * il, acc.w * il);
-    *(u32x2 *)out = v;
+    store_row(acc, l);
 }
 
 }  // namespace
