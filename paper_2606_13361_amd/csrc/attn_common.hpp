@@ -43,20 +43,15 @@ constexpr float kRescaleSlack = 8.f;
 // A lane's weights of one tile summing to at most 2^kRescaleSlack are each at
 // most that: the test that lets a tile skip the row maximum.
 constexpr float kSlackSum = 256.f;
-// A tile whose weights (against the current reference) sum above this share
-// of the row's running sum is "significant": if it also holds a new row
-// maximum, the reference moves to that maximum exactly, so the tile's largest
-// weight is 2^0 = 1, which the 16-bit P operand holds without rounding.  Only
-// weights of at most a quarter of the running sum (or below the reference,
-// as in a plain running maximum) are ever rounded, so a dominant key of a
-// peaky row is never.  On flat rows only the first few tiles of a key range
-// are significant.
+// A tile whose largest weight (against the current reference) exceeds this
+// share of the row's mass so far (running sum plus the tile) is
+// "significant": if it also holds a new row maximum, the reference moves to
+// that maximum exactly, so that weight is 2^0 = 1, which the 16-bit P operand
+// holds without rounding.  Every weight that is rounded then holds at most a
+// quarter of its row's final mass, or lies below the reference (as with a
+// plain running maximum), so a dominant key of a peaky row never is.  On flat
+// rows no key comes near that share after the first tile.
 constexpr float kSignificance = 0.25f;
-// The first tiles (stages) of a key range are significant on almost every
-// row (a tile's weights are about 1/t of the running sum at tile t), so there
-// the kernels take the row maximum before the weights and move the reference
-// to every new maximum, instead of computing the weights twice.
-constexpr int kExactTiles = 5;
 
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
     // v_cvt_pk_bf16_f32: round to nearest even
@@ -163,8 +158,6 @@ __device__ __forceinline__ float pair_sum(float x) {
     const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
     return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
-// true in both lanes of a row when it holds in either
-__device__ __forceinline__ bool pair_any(bool b) { return pair_max(b ? 1.f : 0.f) > 0.f; }
 
 
 // Locate the segment (reader) that owns a linear row-tile index.
@@ -370,9 +363,12 @@ __device__ __forceinline__ void tile_step(RowState<D> &rs, const u32x4 (&qf)[D /
         return lsum;
     };
     float lsum = exps();
-    // a significant tile with a new maximum: reference to that maximum, exactly
-    if (__ballot(mx > rs.m && lsum > kSignificance * rs.l)) {
-        const bool mv = mx > rs.m && pair_any(lsum > kSignificance * rs.l);
+    // a new maximum whose weight exceeds kSignificance of the row's mass:
+    // reference to that maximum, exactly.  The lane test (the lane's weights
+    // above that share of its own mass) holds in the lane that has the key.
+    if (__ballot(mx > rs.m && lsum > kSignificance * (rs.l + lsum))) {
+        const float pmax = __builtin_amdgcn_exp2f(mx - rs.m);
+        const bool mv = mx > rs.m && pmax > kSignificance * pair_sum(rs.l + lsum);
         if (__ballot(mv)) {
             move_reference(rs, mv ? mx : rs.m);
             lsum = exps();

@@ -349,7 +349,7 @@ __global__ __launch_bounds__(THREADS) void attn_cont_kernel(const AttnParams p) 
     // int8 stages and the bf16 stages run in loops of their own
     // the arithmetic of one stage for the column tiles in CM (a bit mask)
     auto compute = [&](auto kind, auto cm, const unsigned char *ks_, const unsigned char *vs_,
-                       int64_t key0, bool early) {
+                       int64_t key0) {
         constexpr bool q8 = decltype(kind)::value;
         constexpr int CM = decltype(cm)::value;
         // S^T for every column tile: each K fragment feeds NCT chains
@@ -407,9 +407,8 @@ __global__ __launch_bounds__(THREADS) void attn_cont_kernel(const AttnParams p) 
 #pragma unroll
             for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s[c][i]);
             mx = pair_max(mx) * c2s;
-            // the first stages: a plain running maximum; later ones: when p
-            // could exceed 2^kRescaleSlack
-            const bool need = mx > rs[c].m + (early ? 0.f : kRescaleSlack);
+            // the first stage, or p could exceed 2^kRescaleSlack
+            const bool need = mx > rs[c].m + kRescaleSlack;
             if (__ballot(need)) move_reference(rs[c], need ? mx : rs[c].m);
             auto exps = [&]() {
                 float lsum = 0.f;
@@ -424,9 +423,12 @@ __global__ __launch_bounds__(THREADS) void attn_cont_kernel(const AttnParams p) 
                 return lsum;
             };
             float lsum = exps();
-            // a significant stage with a new maximum: reference to it, exactly
-            if (!early && __ballot(mx > rs[c].m && lsum > kSignificance * rs[c].l)) {
-                const bool mv = mx > rs[c].m && pair_any(lsum > kSignificance * rs[c].l);
+            // a new maximum whose weight exceeds kSignificance of the row's
+            // mass: reference to that maximum, exactly (the lane test holds
+            // in the lane that has the key)
+            if (__ballot(mx > rs[c].m && lsum > kSignificance * (rs[c].l + lsum))) {
+                const float pmax = __builtin_amdgcn_exp2f(mx - rs[c].m);
+                const bool mv = mx > rs[c].m && pmax > kSignificance * pair_sum(rs[c].l + lsum);
                 if (__ballot(mv)) {
                     move_reference(rs[c], mv ? mx : rs[c].m);
                     lsum = exps();
@@ -488,19 +490,19 @@ __global__ __launch_bounds__(THREADS) void attn_cont_kernel(const AttnParams p) 
         if constexpr (Q8 && !q8) {
             if (!o_scaled) scale_o();
         }
-        compute(kind, std::integral_constant<int, (1 << NCT) - 1>{}, ks_, vs_, key0, t + (sfx_split ? 1 : 0) < kExactTiles);
+        compute(kind, std::integral_constant<int, (1 << NCT) - 1>{}, ks_, vs_, key0);
     };
 
     // the split suffix stage, one column tile per wave (waves 0 .. NCT-1), then a
     // barrier: after it wave 3 may refill its second slot
     if (sfx_split) {
         const int64_t key0 = kb + (int64_t)SKEYS * (nst - 1);
-        if (wave == 0) compute(std::false_type{}, std::integral_constant<int, 1>{}, sfx_lds, sfx_lds + HALF, key0, true);
+        if (wave == 0) compute(std::false_type{}, std::integral_constant<int, 1>{}, sfx_lds, sfx_lds + HALF, key0);
         if constexpr (NCT > 1) {
-            if (wave == 1) compute(std::false_type{}, std::integral_constant<int, 2>{}, sfx_lds, sfx_lds + HALF, key0, true);
+            if (wave == 1) compute(std::false_type{}, std::integral_constant<int, 2>{}, sfx_lds, sfx_lds + HALF, key0);
         }
         if constexpr (NCT > 2) {
-            if (wave == 2) compute(std::false_type{}, std::integral_constant<int, 4>{}, sfx_lds, sfx_lds + HALF, key0, true);
+            if (wave == 2) compute(std::false_type{}, std::integral_constant<int, 4>{}, sfx_lds, sfx_lds + HALF, key0);
         }
         asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
         __builtin_amdgcn_s_barrier();

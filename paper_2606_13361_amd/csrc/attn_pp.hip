@@ -288,9 +288,9 @@ __global__ __launch_bounds__(PP_THREADS) void attn_pp_kernel(const AttnParams p)
         }
         // P against the current reference m first; the row maximum is needed
         // only when some lane's weights sum above 2^kRescaleSlack (then one of
-        // them may exceed it) or above kSignificance of the running sum (a
-        // significant tile: a new maximum there becomes the reference exactly)
-        // -- the first tile (m = -1e30) always, on flat rows the next few
+        // them may exceed it) or above kSignificance of its mass so far (then
+        // one of them may be a significant new maximum) -- the first tile
+        // (m = -1e30) always, on flat rows the next two or three
         auto exps = [&](auto loads) {
             float lsum[4] = {0.f, 0.f, 0.f, 0.f};   // four independent partial sums
 #pragma unroll
@@ -311,20 +311,8 @@ __global__ __launch_bounds__(PP_THREADS) void attn_pp_kernel(const AttnParams p)
                 }
             return (lsum[0] + lsum[1]) + (lsum[2] + lsum[3]);
         };
-        const bool early = t < kExactTiles;
-        if (early) {
-            // a plain running maximum: the reference follows every new maximum
-            float m4[4];
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-                m4[i] = fmaxf(fmaxf(fmaxf(s[0][i], s[0][i + 4]), fmaxf(s[0][i + 8], s[0][i + 12])),
-                              fmaxf(fmaxf(s[1][i], s[1][i + 4]), fmaxf(s[1][i + 8], s[1][i + 12])));
-            const float mx = pair_max(fmaxf(fmaxf(m4[0], m4[1]), fmaxf(m4[2], m4[3]))) * c2;
-            const bool need = mx > rs.m;
-            if (__ballot(need)) move_reference(rs, need ? mx : rs.m);
-        }
         float part = exps(with_loads);
-        if (!early && __ballot(!(part <= kSlackSum) || part > kSignificance * rs.l)) {
+        if (__ballot(!(part <= kSlackSum) || part > kSignificance * (rs.l + part))) {
             // row max as a tree (5 dependent levels)
             float v[32];
 #pragma unroll
@@ -337,7 +325,8 @@ __global__ __launch_bounds__(PP_THREADS) void attn_pp_kernel(const AttnParams p)
 #pragma unroll
                 for (int i = 0; i < w; ++i) v[i] = fmaxf(v[i], v[i + w]);
             const float mx = pair_max(v[0]) * c2;
-            const bool sig = pair_any(part > kSignificance * rs.l);
+            const float pmax = __builtin_amdgcn_exp2f(mx - rs.m);
+            const bool sig = mx > rs.m && pmax > kSignificance * pair_sum(rs.l + part);
             const bool need = mx > rs.m + (sig ? 0.f : kRescaleSlack);
             if (__ballot(need)) {
                 move_reference(rs, need ? mx : rs.m);

@@ -190,9 +190,9 @@ __global__ __launch_bounds__(RTHREADS) void attn_rows_kernel(const AttnParams p)
     // come from two independent accumulation chains (even / odd head-dim
     // steps).  Softmax as in the two-group kernel: weights against the current
     // reference m first, the row maximum only when some lane's weights sum
-    // above 2^kRescaleSlack or above kSignificance of the running sum (the
-    // first stage always, on flat rows the next few).
-    auto stage_step = [&](const unsigned char *ks_, const unsigned char *vs_, bool mask, int lim, bool early) {
+    // above 2^kRescaleSlack or above kSignificance of its mass so far (the
+    // first stage always, on flat rows the next two or three).
+    auto stage_step = [&](const unsigned char *ks_, const unsigned char *vs_, bool mask, int lim) {
         u32x4 kf[D / 16], vf[8];
 #pragma unroll
         for (int ks = 0; ks < D / 16; ++ks) kf[ks] = *(const u32x4 *)(ks_ + ka[ks]);
@@ -235,23 +235,14 @@ __global__ __launch_bounds__(RTHREADS) void attn_rows_kernel(const AttnParams p)
             }
             return ls[0] + ls[1];
         };
-        if (early) {
-            // a plain running maximum on the first stages of the range
-            float mx = fmaxf(fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3])),
-                             fmaxf(fmaxf(sv[4], sv[5]), fmaxf(sv[6], sv[7])));
-            mx = fmaxf(mx, fmaxf(fmaxf(fmaxf(sv[8], sv[9]), fmaxf(sv[10], sv[11])),
-                                 fmaxf(fmaxf(sv[12], sv[13]), fmaxf(sv[14], sv[15]))));
-            mx = pair_max(mx) * c2;
-            const bool need = mx > rs.m;
-            if (__ballot(need)) move_reference(rs, need ? mx : rs.m);
-        }
         float part = exps();
-        if (!early && __ballot(!(part <= kSlackSum) || part > kSignificance * rs.l)) {
+        if (__ballot(!(part <= kSlackSum) || part > kSignificance * (rs.l + part))) {
             float mx = sv[0];
 #pragma unroll
             for (int i = 1; i < 16; ++i) mx = fmaxf(mx, sv[i]);
             mx = pair_max(mx) * c2;
-            const bool sig = pair_any(part > kSignificance * rs.l);
+            const float pmax = __builtin_amdgcn_exp2f(mx - rs.m);
+            const bool sig = mx > rs.m && pmax > kSignificance * pair_sum(rs.l + part);
             const bool need = mx > rs.m + (sig ? 0.f : kRescaleSlack);
             if (__ballot(need)) {
                 move_reference(rs, need ? mx : rs.m);
@@ -287,7 +278,7 @@ __global__ __launch_bounds__(RTHREADS) void attn_rows_kernel(const AttnParams p)
             const bool mask = key0 + SKEYS > cache_end;
             const int64_t vis = min(pos, ke - 1) - key0;
             const int lim = (int)max((int64_t)-1, min(vis, (int64_t)SKEYS));
-            stage_step(ks_, vs_, mask, lim, u < kExactTiles);
+            stage_step(ks_, vs_, mask, lim);
         }
     }
 

@@ -8,9 +8,9 @@ reference m are modelled:
             largest weight seen so far is exactly 1;
   lazy   -- m moves only when a tile's maximum exceeds it by more than 2^8
             (the first tile always): weights up to 2^8, the largest rounded;
-  gated  -- the kernels' rule: a plain running maximum on the first 5 tiles
-            of a key range, then lazy, plus m moves to a new maximum exactly
-            whenever the tile's weights sum above a quarter of the running sum.
+  gated  -- the kernels' rule: lazy, plus m moves to a new maximum exactly
+            whenever that maximum's weight exceeds a quarter of the row's mass
+            so far (running sum plus the tile).
 Each rule is run with the prefill's tiling (64-key tiles from key 0) and the
 continuation's (key splits of 256 keys in 32-key stages taken alternately by
 two states, then the log-sum-exp merge), and the two results are compared at
@@ -27,7 +27,7 @@ import pytest
 
 from harness import workloads as W
 
-SLACK, SIG, EXACT_TILES = 8.0, 0.25, 5
+SLACK, SIG = 8.0, 0.25
 
 
 def bf16(x):
@@ -45,7 +45,6 @@ class Rows:
     """Online-softmax state of R rows (log2 domain, fp32)."""
 
     def __init__(self, R, D):
-        self.t = 0                      # tiles seen
         self.m = np.full(R, -1e30, np.float32)
         self.l = np.zeros(R, np.float32)
         self.o = np.zeros((R, D), np.float32)
@@ -59,17 +58,17 @@ class Rows:
         """s [R, T] fp32 scores (-inf where masked), v [R, T, D]."""
         with np.errstate(over="ignore", invalid="ignore"):
             mx = f32(np.max(s, axis=1) * c2)
-            if rule == "exact" or (rule == "gated" and self.t < EXACT_TILES):
+            if rule == "exact":
                 self.move(mx > self.m, mx)
             else:
                 self.move(mx > self.m + SLACK, mx)
                 if rule == "gated":
                     part = np.exp2(f32(s * c2 - self.m[:, None])).sum(1)
-                    self.move((mx > self.m) & (part > SIG * self.l), mx)
+                    pmax = np.exp2(f32(mx - self.m))
+                    self.move((mx > self.m) & (pmax > SIG * (self.l + part)), mx)
             p = np.exp2(f32(s * c2 - self.m[:, None]))
         self.l = f32(self.l + p.sum(1))
         self.o = f32(self.o + np.einsum("rt,rtd->rd", bf16(p).astype(np.float64), v).astype(np.float32))
-        self.t += 1
 
 
 def attend(q, k, v, pos, heads, plan, rule):
