@@ -160,6 +160,13 @@ __device__ __forceinline__ float pair_sum(float x) {
 }
 
 
+// r / G for the small row indices of a continuation workgroup (0 <= r < 128,
+// 1 <= G <= 128) from inv_g = 1/G in fp32 (within a few ulp): (r + 1/2) / G
+// lies at least 1/(2G) from an integer, far beyond the relative error of a
+// few 2^-24 of the product, so the truncation is exact -- one multiply
+// instead of an integer division.
+__device__ __forceinline__ int div_small(int r, float inv_g) { return (int)(((float)r + 0.5f) * inv_g); }
+
 // Locate the segment (reader) that owns a linear row-tile index.
 __device__ __forceinline__ int find_segment(const AttnParams &p, int tile) {
     int lo = 0, hi = p.n_seg - 1;

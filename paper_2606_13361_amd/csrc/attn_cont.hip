@@ -171,6 +171,7 @@ __global__ __launch_bounds__(THREADS) void attn_cont_kernel(const AttnParams p) 
     const int g = blockIdx.x % p.n_kv_heads;
     const int split = blockIdx.x / p.n_kv_heads;
     const int G = p.group;
+    const float inv_g = __builtin_amdgcn_rcpf((float)G);   // within 1 ulp: enough for div_small
     const int S = p.seg_tok0[1];
     const int R = G * S;                            // <= 32 * NCT
     const int64_t npre = p.n_prefix;
@@ -182,18 +183,6 @@ __global__ __launch_bounds__(THREADS) void attn_cont_kernel(const AttnParams p) 
         ke = last_split ? k_all : min(kb + p.chunk, npre);
     }
 
-    // ---- rows: column tile c, lane column j -> row 32*c + j
-    int64_t pos[NCT];
-    bool valid[NCT];
-    int tok[NCT], head[NCT];
-#pragma unroll
-    for (int c = 0; c < NCT; ++c) {
-        const int r = 32 * c + j;
-        valid[c] = r < R;
-        tok[c] = valid[c] ? r / G : 0;
-        head[c] = g * G + (valid[c] ? r % G : 0);
-        pos[c] = valid[c] ? npre + tok[c] : -1;
-    }
     // ---- stages.  bf16: 32-key stages over [kb, ke).  Q8: n_cst stages of cached
     // keys [kb, ce) (the last one may reach past npre: masked), then the new rows'
     // stages (last split only).  Wave w takes stages w, w+4, ...
@@ -318,14 +307,31 @@ __global__ __launch_bounds__(THREADS) void attn_cont_kernel(const AttnParams p) 
             const int base = 4 * (2 * NCT * wave + i);
             const int row = base + (lane >> 4);
             const int rr = row < R ? row : R - 1;
-            const uint64_t src = q_a + (uint64_t)(rr / G) * qtok_b + (uint64_t)(rr % G) * ROWB +
+            const int tk = div_small(rr, inv_g);
+            const uint64_t src = q_a + (uint64_t)tk * qtok_b + (uint64_t)(rr - tk * G) * ROWB +
                                  16u * (uint32_t)((lane & 15) ^ swz(row));
             dma16((const void *)src, qlds + base * ROWB);
         }
     }
     if (sfx_split && wave == 3) load_stage_to(nst - 1, sfx_lds);
+    if (my_n > 0) load_stage(0);
+
+    // ---- rows: column tile c, lane column j -> row 32*c + j (computed while
+    // the first loads are in flight)
+    int64_t pos[NCT];
+    bool valid[NCT];
+    int tok[NCT], head[NCT];
+#pragma unroll
+    for (int c = 0; c < NCT; ++c) {
+        const int r = 32 * c + j;
+        valid[c] = r < R;
+        const int tk = div_small(r, inv_g);
+        tok[c] = valid[c] ? tk : 0;
+        head[c] = g * G + (valid[c] ? r - tk * G : 0);
+        pos[c] = valid[c] ? npre + tok[c] : -1;
+    }
+
     if (my_n > 0) {
-        load_stage(0);
         if (is_q8(0)) wait_vmcnt<LOADS_Q8>();
         else wait_vmcnt<LOADS>();
     } else {
