@@ -93,9 +93,7 @@ __global__ __launch_bounds__(RTHREADS) void attn_rows_kernel(const AttnParams p)
     const int rw = (R + 3) / 4;
     const int r = rw * rg + j;
     const bool valid = j < rw && r < R;
-    const int tok = valid ? r / G : 0;
-    const int head = g * G + (valid ? r % G : 0);
-    const int64_t pos = valid ? npre + tok : -1;
+    const float inv_g = __builtin_amdgcn_rcpf((float)G);   // within 1 ulp: enough for div_small
 
     // ---- load map: wave w moves K rows 4w..4w+3 and V rows 4w..4w+3 of a stage,
     // one instruction each; lane -> row 4w + lane/16, LDS slot lane%16, global
@@ -132,6 +130,33 @@ __global__ __launch_bounds__(RTHREADS) void attn_rows_kernel(const AttnParams p)
         }
     };
 
+    // ---- prologue: the row groups' query rows into LDS (the stage-parity-0 wave
+    // of each group moves them; swizzled like K; rows past R repeat row R-1,
+    // never stored), then the first NS-2 stages (three iterations); Q is older
+    // than every stage in the loading wave's queue
+    const unsigned char *qlds = smem + RING + rg * QW * ROWB;
+    if (par == 0) {
+        const uint64_t q_a = (uint64_t)(uintptr_t)p.q + (uint64_t)g * G * ROWB;
+        const uint64_t qtok_b = (uint64_t)p.n_q_heads * ROWB;
+        const int nq = (rw + 3) / 4;                 // <= 6
+        for (int i = 0; i < nq; ++i) {
+            const int row = 4 * i + (lane >> 4);     // local row
+            const int rr = min(rw * rg + row, R - 1);
+            const int tk = div_small(rr, inv_g);
+            const uint64_t src = q_a + (uint64_t)tk * qtok_b + (uint64_t)(rr - tk * G) * ROWB +
+                                 16u * (uint32_t)((lane & 15) ^ swz(row));
+            dma16((const void *)src, qlds + 4 * i * ROWB);
+        }
+    }
+    const int pro = min(NS - 2, nst);
+    for (int t = 0; t < pro; ++t) load_stage(t);
+
+    // ---- built while the first loads are in flight: the row's token and
+    // head, and the read maps
+    const int tk = div_small(r, inv_g);
+    const int tok = valid ? tk : 0;
+    const int head = g * G + (valid ? r - tk * G : 0);
+    const int64_t pos = valid ? npre + tok : -1;
     // ---- read maps (per lane, loop invariant), as in the other members
     uint32_t ka[D / 16];
 #pragma unroll
@@ -148,25 +173,6 @@ __global__ __launch_bounds__(RTHREADS) void attn_rows_kernel(const AttnParams p)
             va[h][mt] = (uint32_t)row * ROWB + 16u * (uint32_t)(chunk ^ swz(row)) + 8u * (uint32_t)(l16 & 1);
         }
 
-    // ---- prologue: the row groups' query rows into LDS (the stage-parity-0 wave
-    // of each group moves them; swizzled like K; rows past R repeat row R-1,
-    // never stored), then the first NS-2 stages (three iterations); Q is older
-    // than every stage in the loading wave's queue
-    const unsigned char *qlds = smem + RING + rg * QW * ROWB;
-    if (par == 0) {
-        const uint64_t q_a = (uint64_t)(uintptr_t)p.q + (uint64_t)g * G * ROWB;
-        const uint64_t qtok_b = (uint64_t)p.n_q_heads * ROWB;
-        const int nq = (rw + 3) / 4;                 // <= 6
-        for (int i = 0; i < nq; ++i) {
-            const int row = 4 * i + (lane >> 4);     // local row
-            const int rr = min(rw * rg + row, R - 1);
-            const uint64_t src = q_a + (uint64_t)(rr / G) * qtok_b + (uint64_t)(rr % G) * ROWB +
-                                 16u * (uint32_t)((lane & 15) ^ swz(row));
-            dma16((const void *)src, qlds + 4 * i * ROWB);
-        }
-    }
-    const int pro = min(NS - 2, nst);
-    for (int t = 0; t < pro; ++t) load_stage(t);
     wait_stages(max(pro - 2, 0));                    // Q and stages 0, 1 landed
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");
