@@ -115,6 +115,7 @@ def run_q8(desc, L_art, Lp, S, seed, rows=None):
 @pytest.mark.parametrize("Lp,S,extra", [
     (1, 1, 0), (100, 24, 0), (1000, 1, 7), (3774, 24, 0), (3774, 3, 40), (5000, 17, 0), (257, 24, 1),
     (32768 + 5, 1, 0), (32768 + 2, 24, 9),      # prefixes just past a round length (last split takes the extra keys)
+    (1, 24, 0), (40, 24, 0), (65, 9, 3), (64, 24, 0),   # one or two cached stages
 ])
 def test_continue_q8_matches_oracle(Lp, S, extra):
     say("continue_q8: Lp %d S %d artifact %d" % (Lp, S, Lp + extra))
@@ -125,8 +126,9 @@ def test_continue_q8_matches_oracle(Lp, S, extra):
 
 
 def test_continue_q8_other_group_sizes():
-    """G = 1 (96 rows = 3 column tiles at S = 96) and G = 8."""
-    for Hq, Hkv, S in ((8, 8, 96), (64, 8, 12)):
+    """G = 1 (96 rows = 3 column tiles at S = 96), G = 8, G = 2 (40 and 64 rows, up to 32
+    new tokens) and two kv heads."""
+    for Hq, Hkv, S in ((8, 8, 96), (64, 8, 12), (16, 8, 20), (16, 8, 32), (16, 2, 5)):
         say("continue_q8: Hq %d Hkv %d S %d" % (Hq, Hkv, S))
         desc = kvr.make_desc(Hq, Hkv, 128, kvr.KVR_BF16, 2048)
         got, want, _ = run_q8(desc, 2000, 2000, S, seed=Hq)
