@@ -356,7 +356,9 @@ def timed(torch, stream, fn, iters):
 
 
 def sweep(torch, kvr, A, W, dev, stream, lengths, suffix=None):
-    """Prefill of L+24 vs continuation of 24 over L, L in {1024, 4096, 16384, 32768}."""
+    """Prefill of L+24 vs continuation of 24 over L, L in {1024, 4096, 16384, 32768}, over
+    the bf16 cache and over its int8 artifact; and one token (a decode step's attention)
+    over both."""
     sh = W.QWEN
     Hq, Hkv, D = sh.n_q_heads, sh.n_kv_heads, sh.head_dim
     S = suffix or W.SWEEP_S
@@ -428,6 +430,22 @@ def sweep(torch, kvr, A, W, dev, stream, lengths, suffix=None):
         tc8 = graph_time(torch, stream, lambda: [cont8(i) for i in range(R8)], R8)
         if not torch.equal(oc8, ref8):
             raise RuntimeError("graph replay of the int8 continuation differs from the eager result")
+        # one token (a decode step's attention) over the same caches and artifacts
+        q1, k1, v1 = q[L:L + 1].contiguous(), k[L:L + 1].contiguous(), v[L:L + 1].contiguous()
+        o1, o18 = torch.empty_like(q1), torch.empty_like(q1)
+
+        def dec(i):
+            c = pool[i % R]
+            kvr.kvr_continue(desc, q1, k1, v1, c[0], c[1], L, 1, o1, ws)
+
+        def dec8(i):
+            kq, vq, sc = arts[i % R8]
+            kvr.kvr_continue_q8(desc, q1, k1, v1, kq, vq, sc, L, 1, o18, ws)
+        for i in range(max(R, R8)):
+            dec(i)
+            dec8(i)
+        td = graph_time(torch, stream, lambda: [dec(i) for i in range(R)], R)
+        td8 = graph_time(torch, stream, lambda: [dec8(i) for i in range(R8)], R8)
         del pool, arts
         tp_avg = sum(tp) / len(tp)
         tc_avg = tc
@@ -452,6 +470,10 @@ def sweep(torch, kvr, A, W, dev, stream, lengths, suffix=None):
             "q8_speedup_vs_bf16_cache": round(tc_avg / tc8, 3),
             "q8_maxabs_vs_bf16_cache": round(q8_dev, 5),
             "continue_q8_rotated_artifacts": R8,
+            "decode_us": round(td * 1e6, 2),
+            "decode_hbm_frac": round(A.continue_bytes(L, 1, Hq, Hkv, D, 2) / td / 1e9 / PEAK_HBM_GBPS, 4),
+            "decode_q8_us": round(td8 * 1e6, 2),
+            "q8_decode_speedup_vs_bf16_cache": round(td / td8, 3),
         })
         del q, k, v, out, kc, vc
         torch.cuda.empty_cache()
