@@ -1,6 +1,7 @@
 // attn_cont.hip -- continuation over a long cached prefix (the HBM-bound
 // mode), bf16, head_dim 128, for up to 96 query rows per kv head (G*S <= 96:
-// decode steps and short continuations).
+// decode steps and short continuations; the row-split kernel takes 33..96
+// rows over short key ranges per workgroup), and over the int8 artifact.
 //
 // Split-K inside the workgroup: each of the 4 waves owns ALL query rows of
 // the workgroup (1..3 MFMA column tiles of 32) and a quarter of the keys --

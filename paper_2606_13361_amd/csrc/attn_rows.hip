@@ -1,6 +1,7 @@
 // attn_rows.hip -- continuation over a long cached prefix (the HBM-bound
-// mode), bf16, head_dim 128, for up to 96 query rows per kv head (G*S <= 96:
-// decode steps and short continuations).
+// mode), bf16, head_dim 128, for 33..96 query rows per kv head (short
+// continuations, G*S <= 96) when each workgroup's key range is short (the
+// host routes one-tile decode steps and long ranges to the keys-split kernel).
 //
 // A workgroup owns one key range [kb, ke) of one kv head; the host splits the
 // prefix across workgroups so that about one workgroup runs per CU, and the
