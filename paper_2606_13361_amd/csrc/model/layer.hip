@@ -128,6 +128,15 @@ __global__ __launch_bounds__(NT) void qk_norm_rope_kernel(const QkParams p) {
     }
 }
 
+// silu(g) = g / (1 + e^-g) with the hardware exponential (2^x) and reciprocal
+// (each within about an ulp of fp32): the product with the up row is rounded to
+// the element format, far coarser.  Large -g gives 2^x = inf, rcp = 0, silu = -0.
+// One definition for the multi-row kernel and the one-row prologue, so a
+// continuation step and a prefill give the same activation bits.
+__device__ __forceinline__ float silu(float g) {
+    return g * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(g * -1.4426950408889634f));
+}
+
 // act[t][i] = silu(gu[t][i]) * gu[t][I + i], 8 elements per thread.
 template <class E>
 __global__ __launch_bounds__(NT) void silu_mul_kernel(const uint16_t *gu, uint16_t *act, int64_t T, int I) {
@@ -142,7 +151,7 @@ __global__ __launch_bounds__(NT) void silu_mul_kernel(const uint16_t *gu, uint16
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
             const float g0 = E::lo(g[i]), g1 = E::hi(g[i]);
-            o[i] = E::pack2(g0 / (1.0f + expf(-g0)) * E::lo(u[i]), g1 / (1.0f + expf(-g1)) * E::hi(u[i]));
+            o[i] = E::pack2(silu(g0) * E::lo(u[i]), silu(g1) * E::hi(u[i]));
         }
         *(u32x4 *)(act + t * I + 8 * c) = o;
     }
@@ -174,38 +183,13 @@ struct GemvParams {
 constexpr int GT = 512;            // threads of a one-row-product workgroup
 constexpr int kGemvMaxGrid = 512;  // workgroups: two per compute unit
 
-template <class E, int PRO, int RW>
-__global__ __launch_bounds__(GT) void gemv_kernel(const GemvParams p) {
-    __shared__ __attribute__((aligned(16))) uint16_t xs[kGemvMaxK];
-    __shared__ float red[GT / 64];
-    constexpr int U = RW == 1 ? 8 : 4;                   // k-steps per block of loads
+// x' of a one-row product into LDS (see above), by all GT threads of the workgroup
+template <class E, int PRO>
+__device__ __forceinline__ void build_x(const GemvParams &p, uint16_t *xs, float *red, int tid) {
     constexpr int NW = GT / 64;
-    const int tid = threadIdx.x;
     const int KC = p.K / 8;
     const int wave = tid >> 6, lane = tid & 63;
-    const int steps = (KC + 63) / 64;
-    // wave w of workgroup b takes row groups (b * NW + w) * RW, then every
-    // grid-stride after it: each workgroup builds x' once for all its rows
-    const int64_t stride = (int64_t)gridDim.x * NW * RW;
-    int64_t n0 = ((int64_t)blockIdx.x * NW + wave) * RW;
-    u32x4 wv[U][RW];
-    // Every load is issued, from a clamped (valid) address: without branches
-    // the compiler counts the loads in flight and waits only for the block it
-    // uses.  Chunks past K and rows past N are loaded and never used.
-    auto load_block = [&](int64_t nb, int s0) {
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const int c = min(lane + 64 * (s0 + u), KC - 1);
-#pragma unroll
-            for (int r = 0; r < RW; ++r) {
-                const int64_t row = nb + r < p.N ? nb + r : p.N - 1;
-                wv[u][r] = *(const u32x4 *)(p.w + row * p.K + 8 * c);
-            }
-        }
-    };
-    // the first weights do not depend on x: in flight while the prologue runs
-    load_block(n0, 0);
-
+    (void)wave; (void)lane;
     if (PRO == kNorm) {
         float ss = 0.f;
         for (int c = tid; c < KC; c += GT) {
@@ -242,13 +226,48 @@ __global__ __launch_bounds__(GT) void gemv_kernel(const GemvParams p) {
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
                 const float g0 = E::lo(g[i]), g1 = E::hi(g[i]);
-                o[i] = E::pack2(g0 / (1.0f + expf(-g0)) * E::lo(u[i]), g1 / (1.0f + expf(-g1)) * E::hi(u[i]));
+                o[i] = E::pack2(silu(g0) * E::lo(u[i]), silu(g1) * E::hi(u[i]));
             }
             *(u32x4 *)(xs + 8 * c) = o;
         }
     } else {
         for (int c = tid; c < KC; c += GT) *(u32x4 *)(xs + 8 * c) = *(const u32x4 *)(p.x + 8 * c);
     }
+}
+
+template <class E, int PRO, int RW>
+__global__ __launch_bounds__(GT) void gemv_kernel(const GemvParams p) {
+    __shared__ __attribute__((aligned(16))) uint16_t xs[kGemvMaxK];
+    __shared__ float red[GT / 64];
+    constexpr int U = RW == 1 ? 8 : 4;                   // k-steps per block of loads
+    constexpr int NW = GT / 64;
+    const int tid = threadIdx.x;
+    const int KC = p.K / 8;
+    const int wave = tid >> 6, lane = tid & 63;
+    const int steps = (KC + 63) / 64;
+    // wave w of workgroup b takes row groups (b * NW + w) * RW, then every
+    // grid-stride after it: each workgroup builds x' once for all its rows
+    const int64_t stride = (int64_t)gridDim.x * NW * RW;
+    int64_t n0 = ((int64_t)blockIdx.x * NW + wave) * RW;
+    u32x4 wv[U][RW];
+    // Every load is issued, from a clamped (valid) address: without branches
+    // the compiler counts the loads in flight and waits only for the block it
+    // uses.  Chunks past K and rows past N are loaded and never used.
+    auto load_block = [&](int64_t nb, int s0) {
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int c = min(lane + 64 * (s0 + u), KC - 1);
+#pragma unroll
+            for (int r = 0; r < RW; ++r) {
+                const int64_t row = nb + r < p.N ? nb + r : p.N - 1;
+                wv[u][r] = *(const u32x4 *)(p.w + row * p.K + 8 * c);
+            }
+        }
+    };
+    // the first weights do not depend on x: in flight while the prologue runs
+    load_block(n0, 0);
+
+    build_x<E, PRO>(p, xs, red, tid);
     __syncthreads();
 
     for (; n0 < p.N; n0 += stride) {
@@ -293,6 +312,55 @@ __global__ __launch_bounds__(GT) void gemv_kernel(const GemvParams p) {
             if (p.beta) v += E::lo((uint32_t)p.y[n0 + lane]);
             p.y[n0 + lane] = (uint16_t)(E::pack2(v, 0.f) & 0xffffu);
         }
+    }
+}
+
+// One output row per wave, its whole weight row in one block of U 16-byte
+// loads per lane (U * 64 * 8 >= K), issued right after the prologue's reads of
+// x: every weight byte of the product is requested at once, for outputs of up to
+// kGemv1MaxRows rows (the layer's QKV, O and down products).  The grid-stride
+// kernel above pipelines blocks of 8 and serves the wide products.
+constexpr int64_t kGemv1MaxRows = 8192;
+constexpr int kGemv1MaxSteps = 20;
+
+template <class E, int PRO, int U>
+__global__ __launch_bounds__(GT) void gemv1_kernel(const GemvParams p) {
+    __shared__ __attribute__((aligned(16))) uint16_t xs[kGemvMaxK];
+    __shared__ float red[GT / 64];
+    const int tid = threadIdx.x;
+    const int KC = p.K / 8;
+    const int wave = tid >> 6, lane = tid & 63;
+    const int64_t n = (int64_t)blockIdx.x * (GT / 64) + wave;
+    const int64_t row = n < p.N ? n : p.N - 1;       // past N: loaded, never stored
+    // x' first: a wave's loads complete in issue order, so the prologue's reads
+    // of x issued behind the weights would wait for all of them
+    build_x<E, PRO>(p, xs, red, tid);
+    u32x4 wv[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        const int c = min(lane + 64 * u, KC - 1);    // past K: loaded, never used
+        wv[u] = *(const u32x4 *)(p.w + row * p.K + 8 * c);
+    }
+    __syncthreads();
+    float acc = 0.f;
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        const int c = lane + 64 * u;
+        if (c < KC) {
+            const u32x4 xv = *(const u32x4 *)(xs + 8 * c);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                acc = __builtin_fmaf(E::lo(wv[u][i]), E::lo(xv[i]), acc);
+                acc = __builtin_fmaf(E::hi(wv[u][i]), E::hi(xv[i]), acc);
+            }
+        }
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) acc += __shfl_xor(acc, o);
+    if (lane == 0 && n < p.N) {
+        float v = acc;
+        if (p.beta) v += E::lo((uint32_t)p.y[n]);
+        p.y[n] = (uint16_t)(E::pack2(v, 0.f) & 0xffffu);
     }
 }
 
@@ -365,8 +433,10 @@ int linear(Blas *bl, int32_t dtype, const void *x, const void *w, int64_t rows, 
     return st == HIPBLAS_STATUS_SUCCESS ? KVR_OK : KVR_ERR_DEVICE;
 }
 
-// One-row product: at most kGemvMaxGrid workgroups of GT threads, one row per
-// wave and step (two for outputs of 65536 rows and more).
+// One-row product: up to kGemv1MaxRows outputs with rows of at most
+// kGemv1MaxSteps loads per lane, one row per wave and all loads at once;
+// otherwise at most kGemvMaxGrid workgroups of GT threads, one row per wave and
+// step (two for outputs of 65536 rows and more).
 int gemv(int32_t dtype, int pro, const void *x, const void *ln, float eps, const void *w, int32_t K, int64_t N,
          int beta, void *y, hipStream_t s) {
     GemvParams g;
@@ -378,6 +448,21 @@ int gemv(int32_t dtype, int pro, const void *x, const void *ln, float eps, const
     g.K = K;
     g.beta = beta;
     g.eps = eps;
+    const int steps = (K / 8 + 63) / 64;
+    if (N <= kGemv1MaxRows && steps <= kGemv1MaxSteps) {
+        const dim3 grid1((unsigned)((N + GT / 64 - 1) / (GT / 64)));
+#define KVR_GEMV1(E_, P_, U_) hipLaunchKernelGGL((gemv1_kernel<E_, P_, U_>), grid1, dim3(GT), 0, s, g)
+#define KVR_GEMV1_U(E_, P_) do { if (steps <= 5) KVR_GEMV1(E_, P_, 5); else if (steps <= 8) KVR_GEMV1(E_, P_, 8); \
+                                 else KVR_GEMV1(E_, P_, kGemv1MaxSteps); } while (0)
+#define KVR_GEMV1_PRO(E_) do { if (pro == kNorm) KVR_GEMV1_U(E_, kNorm); else if (pro == kSilu) KVR_GEMV1_U(E_, kSilu); \
+                               else KVR_GEMV1_U(E_, kPlain); } while (0)
+        if (dtype == KVR_F16) KVR_GEMV1_PRO(F16);
+        else KVR_GEMV1_PRO(Bf16);
+#undef KVR_GEMV1_PRO
+#undef KVR_GEMV1_U
+#undef KVR_GEMV1
+        return hipGetLastError() == hipSuccess ? KVR_OK : KVR_ERR_DEVICE;
+    }
     const int rw = N >= 65536 ? 2 : 1;
     const int64_t groups = (N + rw * (GT / 64) - 1) / (rw * (GT / 64));
     const dim3 grid((unsigned)(groups < kGemvMaxGrid ? groups : kGemvMaxGrid));
