@@ -183,16 +183,16 @@ struct GemvParams {
 constexpr int GT = 512;            // threads of a one-row-product workgroup
 constexpr int kGemvMaxGrid = 512;  // workgroups: two per compute unit
 
-// x' of a one-row product into LDS (see above), by all GT threads of the workgroup
-template <class E, int PRO>
+// x' of a one-row product into LDS (see above), by all NTH threads of the workgroup
+template <class E, int PRO, int NTH>
 __device__ __forceinline__ void build_x(const GemvParams &p, uint16_t *xs, float *red, int tid) {
-    constexpr int NW = GT / 64;
+    constexpr int NW = NTH / 64;
     const int KC = p.K / 8;
     const int wave = tid >> 6, lane = tid & 63;
     (void)wave; (void)lane;
     if (PRO == kNorm) {
         float ss = 0.f;
-        for (int c = tid; c < KC; c += GT) {
+        for (int c = tid; c < KC; c += NTH) {
             const u32x4 v = *(const u32x4 *)(p.x + 8 * c);
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
@@ -209,7 +209,7 @@ __device__ __forceinline__ void build_x(const GemvParams &p, uint16_t *xs, float
 #pragma unroll
         for (int i = 0; i < NW; ++i) tot += red[i];
         const float inv = 1.0f / sqrtf(tot / (float)p.K + p.eps);
-        for (int c = tid; c < KC; c += GT) {
+        for (int c = tid; c < KC; c += NTH) {
             const u32x4 v = *(const u32x4 *)(p.x + 8 * c);
             const u32x4 g = *(const u32x4 *)(p.ln + 8 * c);
             u32x4 o;
@@ -219,7 +219,7 @@ __device__ __forceinline__ void build_x(const GemvParams &p, uint16_t *xs, float
             *(u32x4 *)(xs + 8 * c) = o;
         }
     } else if (PRO == kSilu) {
-        for (int c = tid; c < KC; c += GT) {
+        for (int c = tid; c < KC; c += NTH) {
             const u32x4 g = *(const u32x4 *)(p.x + 8 * c);
             const u32x4 u = *(const u32x4 *)(p.x + p.K + 8 * c);
             u32x4 o;
@@ -231,24 +231,30 @@ __device__ __forceinline__ void build_x(const GemvParams &p, uint16_t *xs, float
             *(u32x4 *)(xs + 8 * c) = o;
         }
     } else {
-        for (int c = tid; c < KC; c += GT) *(u32x4 *)(xs + 8 * c) = *(const u32x4 *)(p.x + 8 * c);
+        for (int c = tid; c < KC; c += NTH) *(u32x4 *)(xs + 8 * c) = *(const u32x4 *)(p.x + 8 * c);
     }
 }
 
-template <class E, int PRO, int RW>
+// PAIR (RW = 2): the weights hold 2N rows, gate rows 0..N-1 then up rows
+// N..2N-1; a wave takes the pair (n, N + n) and stores act[n] =
+// silu(g) * u with g and u rounded to the element format first, as the
+// multi-row path rounds them before silu_mul_kernel.
+template <class E, int PRO, int RW, int PAIR = 0>
 __global__ __launch_bounds__(GT) void gemv_kernel(const GemvParams p) {
+    static_assert(!PAIR || RW == 2, "a pair is two rows");
     __shared__ __attribute__((aligned(16))) uint16_t xs[kGemvMaxK];
     __shared__ float red[GT / 64];
     constexpr int U = RW == 1 ? 8 : 4;                   // k-steps per block of loads
     constexpr int NW = GT / 64;
+    constexpr int RPW = PAIR ? 1 : RW;                   // outputs per wave and step
     const int tid = threadIdx.x;
     const int KC = p.K / 8;
     const int wave = tid >> 6, lane = tid & 63;
     const int steps = (KC + 63) / 64;
-    // wave w of workgroup b takes row groups (b * NW + w) * RW, then every
+    // wave w of workgroup b takes row groups (b * NW + w) * RPW, then every
     // grid-stride after it: each workgroup builds x' once for all its rows
-    const int64_t stride = (int64_t)gridDim.x * NW * RW;
-    int64_t n0 = ((int64_t)blockIdx.x * NW + wave) * RW;
+    const int64_t stride = (int64_t)gridDim.x * NW * RPW;
+    int64_t n0 = ((int64_t)blockIdx.x * NW + wave) * RPW;
     u32x4 wv[U][RW];
     // Every load is issued, from a clamped (valid) address: without branches
     // the compiler counts the loads in flight and waits only for the block it
@@ -259,7 +265,8 @@ __global__ __launch_bounds__(GT) void gemv_kernel(const GemvParams p) {
             const int c = min(lane + 64 * (s0 + u), KC - 1);
 #pragma unroll
             for (int r = 0; r < RW; ++r) {
-                const int64_t row = nb + r < p.N ? nb + r : p.N - 1;
+                const int64_t row = PAIR ? (nb < p.N ? nb : p.N - 1) + r * p.N
+                                         : (nb + r < p.N ? nb + r : p.N - 1);
                 wv[u][r] = *(const u32x4 *)(p.w + row * p.K + 8 * c);
             }
         }
@@ -267,11 +274,11 @@ __global__ __launch_bounds__(GT) void gemv_kernel(const GemvParams p) {
     // the first weights do not depend on x: in flight while the prologue runs
     load_block(n0, 0);
 
-    build_x<E, PRO>(p, xs, red, tid);
+    build_x<E, PRO, GT>(p, xs, red, tid);
     __syncthreads();
 
     for (; n0 < p.N; n0 += stride) {
-        const int rows = p.N - n0 < RW ? (int)(p.N - n0) : RW;
+        const int rows = p.N - n0 < RPW ? (int)(p.N - n0) : RPW;
         float acc[RW];
 #pragma unroll
         for (int r = 0; r < RW; ++r) acc[r] = 0.f;
@@ -304,7 +311,12 @@ __global__ __launch_bounds__(GT) void gemv_kernel(const GemvParams p) {
         for (int r = 0; r < RW; ++r)
 #pragma unroll
             for (int o = 32; o > 0; o >>= 1) acc[r] += __shfl_xor(acc[r], o);
-        if (lane < rows) {
+        if constexpr (PAIR) {
+            if (lane == 0) {
+                const float g = E::lo(E::pack2(acc[0], 0.f)), u = E::lo(E::pack2(acc[1], 0.f));
+                p.y[n0] = (uint16_t)(E::pack2(silu(g) * u, 0.f) & 0xffffu);
+            }
+        } else if (lane < rows) {
             float v = acc[0];
 #pragma unroll
             for (int r = 1; r < RW; ++r)
@@ -321,25 +333,40 @@ __global__ __launch_bounds__(GT) void gemv_kernel(const GemvParams p) {
 // kGemv1MaxRows rows (the layer's QKV, O and down products).  The grid-stride
 // kernel above pipelines blocks of 8 and serves the wide products.
 constexpr int64_t kGemv1MaxRows = 8192;
-constexpr int kGemv1MaxSteps = 20;
+constexpr int64_t kGemv1Cus = 256;    // compute units of the part (MI355X)
+constexpr int kGemv1MaxSteps = 19;   // K = 9728 (the Qwen3-4B MLP width) exactly
 
-template <class E, int PRO, int U>
-__global__ __launch_bounds__(GT) void gemv1_kernel(const GemvParams p) {
+template <class E, int PRO, int U, int NWV>
+__global__ __launch_bounds__(64 * NWV) void gemv1_kernel(const GemvParams p) {
+    constexpr int NTH = 64 * NWV;
     __shared__ __attribute__((aligned(16))) uint16_t xs[kGemvMaxK];
-    __shared__ float red[GT / 64];
+    __shared__ float red[NWV];
     const int tid = threadIdx.x;
     const int KC = p.K / 8;
     const int wave = tid >> 6, lane = tid & 63;
-    const int64_t n = (int64_t)blockIdx.x * (GT / 64) + wave;
+    const int64_t n = (int64_t)blockIdx.x * NWV + wave;
     const int64_t row = n < p.N ? n : p.N - 1;       // past N: loaded, never stored
     // x' first: a wave's loads complete in issue order, so the prologue's reads
-    // of x issued behind the weights would wait for all of them
-    build_x<E, PRO>(p, xs, red, tid);
+    // of x issued behind the weights would wait for all of them.  A plain x is
+    // read into registers, the weights requested, and x stored to LDS after.
+    constexpr int XR = (64 * U + NTH - 1) / NTH;     // x chunks per thread (K <= 512 U)
+    u32x4 xr[XR];
+    if constexpr (PRO == kPlain) {
+#pragma unroll
+        for (int i = 0; i < XR; ++i) xr[i] = *(const u32x4 *)(p.x + 8 * min(tid + NTH * i, KC - 1));
+    } else {
+        build_x<E, PRO, NTH>(p, xs, red, tid);
+    }
     u32x4 wv[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
         const int c = min(lane + 64 * u, KC - 1);    // past K: loaded, never used
         wv[u] = *(const u32x4 *)(p.w + row * p.K + 8 * c);
+    }
+    if constexpr (PRO == kPlain) {
+#pragma unroll
+        for (int i = 0; i < XR; ++i)
+            if (tid + NTH * i < KC) *(u32x4 *)(xs + 8 * (tid + NTH * i)) = xr[i];
     }
     __syncthreads();
     float acc = 0.f;
@@ -450,8 +477,20 @@ int gemv(int32_t dtype, int pro, const void *x, const void *ln, float eps, const
     g.eps = eps;
     const int steps = (K / 8 + 63) / 64;
     if (N <= kGemv1MaxRows && steps <= kGemv1MaxSteps) {
-        const dim3 grid1((unsigned)((N + GT / 64 - 1) / (GT / 64)));
-#define KVR_GEMV1(E_, P_, U_) hipLaunchKernelGGL((gemv1_kernel<E_, P_, U_>), grid1, dim3(GT), 0, s, g)
+        // waves per workgroup: the fewest rows on the busiest CU (kGemv1Cus
+        // compute units, one workgroup each per round), ties to the larger
+        // workgroup (fewer prologues): 2560 rows -> 10 waves, 6144 -> 12
+        int nwv = 8;
+        int64_t best = -1;
+        for (const int c : {8, 10, 12, 16}) {
+            const int64_t wgs = (N + c - 1) / c;
+            const int64_t busiest = (wgs + kGemv1Cus - 1) / kGemv1Cus * c;
+            if (best < 0 || busiest <= best) { best = busiest; nwv = c; }
+        }
+        const dim3 grid1((unsigned)((N + nwv - 1) / nwv));
+#define KVR_GEMV1_W(E_, P_, U_, W_) hipLaunchKernelGGL((gemv1_kernel<E_, P_, U_, W_>), grid1, dim3(64 * W_), 0, s, g)
+#define KVR_GEMV1(E_, P_, U_) do { if (nwv == 10) KVR_GEMV1_W(E_, P_, U_, 10); else if (nwv == 12) KVR_GEMV1_W(E_, P_, U_, 12); \
+                                   else if (nwv == 16) KVR_GEMV1_W(E_, P_, U_, 16); else KVR_GEMV1_W(E_, P_, U_, 8); } while (0)
 #define KVR_GEMV1_U(E_, P_) do { if (steps <= 5) KVR_GEMV1(E_, P_, 5); else if (steps <= 8) KVR_GEMV1(E_, P_, 8); \
                                  else KVR_GEMV1(E_, P_, kGemv1MaxSteps); } while (0)
 #define KVR_GEMV1_PRO(E_) do { if (pro == kNorm) KVR_GEMV1_U(E_, kNorm); else if (pro == kSilu) KVR_GEMV1_U(E_, kSilu); \
@@ -461,6 +500,7 @@ int gemv(int32_t dtype, int pro, const void *x, const void *ln, float eps, const
 #undef KVR_GEMV1_PRO
 #undef KVR_GEMV1_U
 #undef KVR_GEMV1
+#undef KVR_GEMV1_W
         return hipGetLastError() == hipSuccess ? KVR_OK : KVR_ERR_DEVICE;
     }
     const int rw = N >= 65536 ? 2 : 1;
@@ -475,6 +515,26 @@ int gemv(int32_t dtype, int pro, const void *x, const void *ln, float eps, const
 #undef KVR_GEMV_PRO
 #undef KVR_GEMV_RW
 #undef KVR_GEMV
+    return hipGetLastError() == hipSuccess ? KVR_OK : KVR_ERR_DEVICE;
+}
+
+// act[n] = silu(x' wg[n]) * (x' wg[I + n]) for one row x, x' = rmsnorm(x) * ln:
+// the gate and up products of the one-token step, paired in each wave.
+int gemv_gate_up(int32_t dtype, const void *x, const void *ln, float eps, const void *w, int32_t K, int64_t I,
+                 void *act, hipStream_t s) {
+    GemvParams g;
+    g.x = (const uint16_t *)x;
+    g.w = (const uint16_t *)w;
+    g.ln = (const uint16_t *)ln;
+    g.y = (uint16_t *)act;
+    g.N = I;
+    g.K = K;
+    g.beta = 0;
+    g.eps = eps;
+    const int64_t groups = (I + GT / 64 - 1) / (GT / 64);
+    const dim3 grid((unsigned)(groups < kGemvMaxGrid ? groups : kGemvMaxGrid));
+    if (dtype == KVR_F16) hipLaunchKernelGGL((gemv_kernel<F16, kNorm, 2, 1>), grid, dim3(GT), 0, s, g);
+    else hipLaunchKernelGGL((gemv_kernel<Bf16, kNorm, 2, 1>), grid, dim3(GT), 0, s, g);
     return hipGetLastError() == hipSuccess ? KVR_OK : KVR_ERR_DEVICE;
 }
 
@@ -660,8 +720,8 @@ int kvr_layer_forward(const kvr_desc *desc, const kvr_layer_shape *shape, const 
         return st;
     // MLP block
     if (one) {
-        if ((st = gemv(dt, kNorm, h, w->ln2, shape->eps, w->wgu, H, 2 * I, 0, b + lw.gu, s))) return st;
-        return gemv(dt, kSilu, b + lw.gu, nullptr, 0.f, w->wd, I, H, 1, h, s);
+        if ((st = gemv_gate_up(dt, h, w->ln2, shape->eps, w->wgu, H, I, b + lw.act, s))) return st;
+        return gemv(dt, kPlain, b + lw.act, nullptr, 0.f, w->wd, I, H, 1, h, s);
     }
     if ((st = kvr_rmsnorm(dt, h, w->ln2, T, H, shape->eps, b + lw.xn, stream))) return st;
     if ((st = linear(bl, dt, b + lw.xn, w->wgu, T, H, 2 * I, 0.f, b + lw.gu, blws, KVR_BLAS_WORKSPACE_BYTES, s)))
