@@ -18,8 +18,10 @@ serve them.
 
 After the timed steps, the length sweep (prefix 1024 / 4096 / 16384 / 32768,
 S = 24, continuations graph-replayed over rotated caches), the 36-layer
-decode chain (32768-token caches, 24 steps of S=1) and a CPU-oracle baseline
-on a bounded sample of the 32792-token prefill are measured.
+decode chain (32768-token caches, 24 steps of S=1), 2..64 readers of the
+3774-token prefix in one call against the same continuations one by one,
+and a CPU-oracle baseline on a bounded sample of the 32792-token prefill are
+measured.
 
 Prints ONE JSON line.
 """
@@ -49,6 +51,7 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-artifact", action="store_true")
     ap.add_argument("--no-rope", action="store_true")
+    ap.add_argument("--no-readers-sweep", action="store_true")
     ap.add_argument("--no-model", action="store_true",
                     help="skip the random-weight 36-layer model (Table 1's prefill vs continuation step)")
     ap.add_argument("--model-only", action="store_true")
@@ -127,6 +130,7 @@ def main():
     cu = W.cu_seqlens(lens)
     rq, rk, rv = W.qkv_device(cu[-1], sh, seed=1, device=dev)
     rout = torch.empty_like(rq)
+    ws_rd = kvr.workspace_for(desc_r, Lr, cu[-1], len(cu) - 1)
     dq, dk, dv = W.qkv_device(1, sh, seed=2, device=dev)
     dout = torch.empty_like(dq)
     ws_dec = kvr.workspace_for(desc32, L32, 1)
@@ -149,7 +153,7 @@ def main():
         rec(3)
         kvr.kvr_cache_append(desc32, ks, vs, S, c_new[0], c_new[1], L32)
         rec(4)
-        kvr.kvr_continue_batched(desc_r, rq, rk, rv, cu, kc_r, vc_r, Lr, rout)
+        kvr.kvr_continue_batched(desc_r, rq, rk, rv, cu, kc_r, vc_r, Lr, rout, ws_rd)
         rec(5)
         kvr.kvr_continue_append(desc32, dq, dk, dv, c_old[0], c_old[1], L32, 1, dout, ws_dec)
         rec(6)
@@ -261,7 +265,8 @@ def main():
                             c32_bytes, avg["continue32k"]),
         "continue16k": roof("continue16k", "attn_rows_kernel + merge_bf16_kernel<128>", "hbm", c16_gbps,
                             c16_bytes, avg["continue16k"]),
-        "readers": roof("readers", "attn_pp_kernel<readers>", "mfma", rd_tflops, rd_flops, avg["readers"]),
+        "readers": roof("readers", "attn_pp_kernel<readers> + merge_bf16_kernel<128>", "mfma", rd_tflops, rd_flops,
+                        avg["readers"]),
         "decode_step": roof("decode_step", "attn_cont_kernel<1> + merge_bf16_kernel<128>", "hbm",
                             dec_bytes / avg["decode_step"] / 1e9, dec_bytes, avg["decode_step"]),
     }
@@ -281,6 +286,8 @@ def main():
         result["artifact"] = artifact(torch, kvr, W, dev, stream)
     if not args.no_rope:
         result["rope"] = rope_calls(torch, kvr, A, W, dev, stream)
+    if not args.no_readers_sweep:
+        result["readers_sweep"] = readers_sweep(torch, kvr, A, W, dev, stream)
     if not args.no_model:
         result["model"] = model_table1(torch, A, W, dev)
     if not args.no_cpu_baseline:
@@ -579,6 +586,56 @@ def artifact(torch, kvr, W, dev, stream):
     return res
 
 
+def readers_sweep(torch, kvr, A, W, dev, stream, counts=(2, 4, 8, 16, 32, 64)):
+    """N readers (S ~ U[24, 256], seeded) of one cached 3774-token prefix in one
+    kvr_continue_batched call, against the same N continuations issued one by
+    one (kvr_continue, each with its own key-split plan); medians of 3 x 10
+    calls, alternated so that both see the same clock."""
+    sh = W.QWEN
+    Hq, Hkv, D = sh.n_q_heads, sh.n_kv_heads, sh.head_dim
+    L = W.READERS_L
+    desc = kvr.make_desc(Hq, Hkv, D, torch.bfloat16, L)
+    g = torch.Generator(device=dev)
+    g.manual_seed(11)
+    kc = torch.randn((Hkv, L, D), generator=g, device=dev).to(torch.bfloat16)
+    vc = torch.randn((Hkv, L, D), generator=g, device=dev).to(torch.bfloat16)
+    rows = []
+    for n in counts:
+        lens = W.reader_lengths(n=n, seed=0)
+        cu = W.cu_seqlens(lens)
+        q, k, v = (x.to(torch.bfloat16) for x in W.qkv_device(cu[-1], sh, seed=n, device=dev))
+        out = torch.empty_like(q)
+        ws = kvr.workspace_for(desc, L, cu[-1], n)
+        parts = [(q[a:b], k[a:b], v[a:b], out[a:b], kvr.workspace_for(desc, L, b - a))
+                 for a, b in zip(cu[:-1], cu[1:])]
+
+        def batched():
+            kvr.kvr_continue_batched(desc, q, k, v, cu, kc, vc, L, out, ws)
+
+        def singles():
+            for (qi, ki, vi, oi, wi) in parts:
+                kvr.kvr_continue(desc, qi, ki, vi, kc, vc, L, qi.shape[0], oi, wi)
+
+        for f in (batched, singles):
+            for _ in range(3):
+                f()
+        torch.cuda.synchronize()
+        tb, ts = [], []
+        for _ in range(3):
+            tb += timed(torch, stream, lambda i: batched(), 10)
+            ts += timed(torch, stream, lambda i: singles(), 10)
+        t_b, t_s = sorted(tb)[len(tb) // 2], sorted(ts)[len(ts) // 2]
+        fl = A.batched_flops(L, lens, Hq, D)
+        rows.append({"readers": n, "tokens": cu[-1], "ms": round(t_b * 1e3, 4),
+                     "tflops": round(fl / t_b / 1e12, 1), "mfma_frac": round(fl / t_b / 1e12 / PEAK_BF16_TFLOPS, 4),
+                     "key_split": ws is not None, "singles_ms": round(t_s * 1e3, 4),
+                     "batched_speedup_vs_singles": round(t_s / t_b, 2)})
+        del q, k, v, out, parts, ws
+    del kc, vc
+    torch.cuda.empty_cache()
+    return rows
+
+
 def rope_calls(torch, kvr, A, W, dev, stream):
     """The step's calls with fused RoPE (positions 0.. for the prefill, L.. for
     the continuations) next to the same calls without it, alternated in blocks
@@ -601,6 +658,7 @@ def rope_calls(torch, kvr, A, W, dev, stream):
     rq, rk, rv = (x.to(dev) for x in W.qkv(cu[-1], sh, seed=1))
     ro = torch.empty_like(rq)
     ws_rd = kvr.workspace_for_rope(desc, L, cu[-1], len(lens))
+    ws_rp = kvr.workspace_for(desc, L, cu[-1], len(lens))
     dq, dk, dv = (x.to(dev) for x in W.qkv(1, sh, seed=2))
     do = torch.empty_like(dq)
     ws_d, ws_dr = kvr.workspace_for(desc, n, 1), kvr.workspace_for_rope(desc, n, 1)
@@ -609,7 +667,7 @@ def rope_calls(torch, kvr, A, W, dev, stream):
                     lambda: kvr.kvr_prefill_rope(desc, tab, q, k, v, n, out_r, kc2, vc2)),
         "continue": (lambda: kvr.kvr_continue(desc, qs, ks, vs, kc, vc, L, S, oc, ws),
                      lambda: kvr.kvr_continue_rope(desc, tab, qs, ks, vs, kc2, vc2, L, S, oc_r, ws_r)),
-        "readers": (lambda: kvr.kvr_continue_batched(desc, rq, rk, rv, cu, kc, vc, L, ro),
+        "readers": (lambda: kvr.kvr_continue_batched(desc, rq, rk, rv, cu, kc, vc, L, ro, ws_rp),
                     lambda: kvr.kvr_continue_batched_rope(desc, tab, rq, rk, rv, cu, kc2, vc2, L, ro, ws_rd)),
         "decode_step": (lambda: (kvr.kvr_continue(desc, dq, dk, dv, kc, vc, n, 1, do, ws_d),
                                  kvr.kvr_cache_append(desc, dk, dv, 1, kc, vc, n)),

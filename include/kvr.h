@@ -147,7 +147,11 @@ int kvr_continue_noalloc(const kvr_desc *desc, const void *Qs, const void *Ks, c
  *   positions L_prefix .. L_prefix + (cu[r+1]-cu[r]) - 1 and see the shared
  *   prefix plus their own rows causally, never another reader's rows.
  *   cu_seqlens_host: HOST array of n+1 int32, cu[0] == 0, non-decreasing.
- *   ws as for kvr_continue with kvr_workspace_bytes(desc, L_prefix, cu[n], n).
+ *   ws: device workspace of at least kvr_workspace_bytes(desc, L_prefix,
+ *   cu[n], n) bytes (16-byte aligned; may be NULL when that is 0).  At bf16 /
+ *   fp16 and head_dim 128, for 2..128 readers, the call may split the row
+ *   tiles of its last partial round of workgroups over the prefix keys and
+ *   merge them through ws.  KVR_ERR_WORKSPACE if ws_bytes is smaller.
  */
 int kvr_continue_batched(const kvr_desc *desc, const void *Qs, const void *Ks, const void *Vs,
                          const int32_t *cu_seqlens_host, int32_t n, const void *kcache,

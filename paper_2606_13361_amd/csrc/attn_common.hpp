@@ -177,6 +177,18 @@ __device__ __forceinline__ int find_segment(const AttnParams &p, int tile) {
     return lo;
 }
 
+// The segment (reader) that holds packed token t: the last of segments
+// [first, n_seg) whose first token is at most t (segments are non-empty, so
+// their first tokens increase).
+__device__ __forceinline__ int segment_of_token(const AttnParams &p, int t, int first) {
+    int lo = first, hi = p.n_seg - 1;
+    while (lo < hi) {
+        int mid = (lo + hi + 1) >> 1;
+        if (p.seg_tok0[mid] <= t) lo = mid; else hi = mid - 1;
+    }
+    return lo;
+}
+
 // What one workgroup computes: 128 rows (token-major (token, head) pairs of
 // kv head g) of one segment, over keys [kb, ke).
 struct Work {

@@ -66,20 +66,47 @@ __global__ __launch_bounds__(PP_THREADS) void attn_pp_kernel(const AttnParams p)
     const int grp = lane >> 5;
 
     // ---- work: kv head fastest (XCD locality); prefill row tiles longest first.
-    // Keys are the cached prefix [0, npre) (readers) followed by the segment's own
-    // rows; prefill has no prefix.
+    // Keys are the cached prefix [0, npre) (readers) followed by own rows from
+    // token tok0 on; prefill has no prefix.
+    //
+    // Readers: the rows of all readers of the launch are packed (G rows per
+    // token, token-major) and cut into tiles of kRowsPP rows regardless of
+    // where a reader ends, since every reader sees the same prefix.  A tile's
+    // own keys start at the first token of the reader that holds its first row
+    // (tok0); a row of a later reader in the tile must not see the own keys
+    // before its reader's first token, keys [npre, lo) in its frame.  Tiles
+    // from tail_tile0 on run as nsplit workgroups each, over equal shares of
+    // the tile's key tiles, and leave fp32 partials for the merge kernel.
     const int G = p.group;
     const int g = blockIdx.x % p.n_kv_heads;
-    const int tile_lin = MODE == kModePrefill ? p.tiles_total - 1 - blockIdx.x / p.n_kv_heads
-                                              : blockIdx.x / p.n_kv_heads;
-    const int seg = MODE == kModeReaders ? find_segment(p, tile_lin) : 0;
-    const int tok0 = p.seg_tok0[seg];
-    const int R = G * (p.seg_tok0[seg + 1] - tok0);
-    const int row0 = (tile_lin - p.seg_tile0[seg]) * kRowsPP;
+    const int bh = blockIdx.x / p.n_kv_heads;
+    int tile_lin, split = 0, nsplit = 1, tok0, R, row0;
+    if constexpr (MODE == kModePrefill) {
+        tile_lin = p.tiles_total - 1 - bh;
+        tok0 = 0;
+        R = G * p.seg_tok0[1];
+        row0 = tile_lin * kRowsPP;
+    } else {
+        if (bh < p.tail_tile0) {
+            tile_lin = bh;
+        } else {
+            nsplit = p.nsplit;
+            split = (bh - p.tail_tile0) % nsplit;
+            tile_lin = p.tail_tile0 + (bh - p.tail_tile0) / nsplit;
+        }
+        const int T0 = p.seg_tok0[0];
+        const int prow0 = tile_lin * kRowsPP;                 // packed row of the launch
+        tok0 = p.seg_tok0[segment_of_token(p, T0 + prow0 / G, 0)];
+        R = G * (p.seg_tok0[p.n_seg] - tok0);
+        row0 = prow0 - G * (tok0 - T0);
+    }
     const int row_last = min(row0 + kRowsPP, R) - 1;
     const int npre = MODE == kModePrefill ? 0 : (int)p.n_prefix;
     const int ke = npre + row_last / G + 1;                       // keys any row here may see
     const int ntiles = (ke + KEYS - 1) / KEYS;
+    // this workgroup's key tiles [tb, te)
+    const int tb = MODE == kModePrefill ? 0 : split * ntiles / nsplit;
+    const int te = MODE == kModePrefill ? ntiles : (split + 1) * ntiles / nsplit;
 
     // rows 32*slot .. +31 of the tile, slot 2*(wave & 3) + group: a partial tile
     // keeps both waves of a SIMD busy as long as it can
@@ -91,6 +118,19 @@ __global__ __launch_bounds__(PP_THREADS) void attn_pp_kernel(const AttnParams p)
     const int pos = valid ? npre + tok : -1;
     const bool wave_active = wrow0 < R;
     const int k_full = wave_active ? npre + wrow0 / G + 1 : 0;   // keys every row of this wave sees
+    // readers: the row's hole [npre, lo) (empty for rows of the tile's first
+    // reader), the wave's largest lo, and the row's own position for RoPE
+    int lo = npre, hole_end = npre;
+    if constexpr (MODE == kModeReaders) {
+        const int t_abs = tok0 + tok;
+        lo = npre + (p.seg_tok0[segment_of_token(p, t_abs, 0)] - tok0);
+        if (!valid) lo = npre;
+        int m = lo;
+#pragma unroll
+        for (int x = 1; x < 64; x <<= 1) m = max(m, __shfl_xor(m, x));
+        hole_end = __builtin_amdgcn_readfirstlane(m);
+    }
+    const int rope_pos = pos - (lo - npre);
 
     u32x4 qf[D / 16];
     {
@@ -99,7 +139,7 @@ __global__ __launch_bounds__(PP_THREADS) void attn_pp_kernel(const AttnParams p)
         for (int ks = 0; ks < D / 16; ++ks)
             qf[ks] = valid ? *(const u32x4 *)(qrow + 16 * ks + 8 * grp) : (u32x4){0, 0, 0, 0};
         // RoPE: the row is rotated once, at its own position
-        if (p.rope && valid) rope_q_frag<E, D>(qf, p.rope + (int64_t)pos * D, grp);
+        if (p.rope && valid) rope_q_frag<E, D>(qf, p.rope + (int64_t)rope_pos * D, grp);
     }
 
     // ---- load map: wave w moves K rows 8w..8w+7 and V rows 8w..8w+7 of a tile,
@@ -203,7 +243,7 @@ __global__ __launch_bounds__(PP_THREADS) void attn_pp_kernel(const AttnParams p)
         pf[st][0] = pf[st][1] = (u32x4){0, 0, 0, 0};
     }
 
-    // GEMM(t): O += V_{t-1} P_{t-1} (t >= 1), S_t = K_t Q^T (t < ntiles), as 8
+    // GEMM(t): O += V_{t-1} P_{t-1} (t > tb), S_t = K_t Q^T (t < te), as 8
     // chunks of 2 S and 2 PV MFMAs; chunk c+1's LDS fragments are read while
     // chunk c's MFMAs run, and nothing moves across chunks (bounded registers)
     auto kfrag = [&](const unsigned char *ks_, int st, int ks) {
@@ -276,14 +316,19 @@ __global__ __launch_bounds__(PP_THREADS) void attn_pp_kernel(const AttnParams p)
     auto soft = [&](auto with_loads, int t, const TileSrc &f) {   // with_loads: the step's
                                                                    // loads among the exps
         const int k0 = t * KEYS;
-        if (k0 + KEYS > k_full) {
+        const bool in_hole = MODE == kModeReaders && k0 < hole_end && k0 + KEYS > npre;
+        if (k0 + KEYS > k_full || in_hole) {
             const int lim = max(-1, min(pos - k0, KEYS));
+            // the hole [npre, lo) as tile offsets [h0, h0 + hn): one unsigned compare
+            const int h0 = npre - k0;
+            const unsigned hn = (unsigned)(lo - npre);
 #pragma unroll
             for (int st = 0; st < 2; ++st)
 #pragma unroll
                 for (int i = 0; i < 16; ++i) {
                     const int o = 32 * st + 8 * (i >> 2) + 4 * grp + (i & 3);
-                    if (o > lim) s[st][i] = -INFINITY;
+                    const bool dead = (o > lim) | ((unsigned)(o - h0) < hn);   // no short circuit: selects, not branches
+                    s[st][i] = dead ? -INFINITY : s[st][i];
                 }
         }
         // P against the current reference m first; the row maximum is needed
@@ -336,16 +381,17 @@ __global__ __launch_bounds__(PP_THREADS) void attn_pp_kernel(const AttnParams p)
         rs.l += part;
     };
 
-    // ---- steps.  Phase 2t starts once tile t has landed (each wave waits for its
-    // own loads, then the barrier); during phase 2t every wave issues its loads
-    // of tile t+2, spread through its step, into the stage that held tile t-2
-    // (last read in phase 2t-1).  Group A: GEMM(t) in phase 2t, SOFT(t)
-    // in phase 2t+1; group B one phase later.  Both run 2*ntiles + 2 phases.
+    // ---- steps, over key tiles [tb, te), phases counted from tb.  Phase 2u
+    // starts once tile tb+u has landed (each wave waits for its own loads, then
+    // the barrier); during phase 2u every wave issues its loads of tile tb+u+2,
+    // spread through its step, into the stage that held tile tb+u-2 (last read
+    // in phase 2u-1).  Group A: GEMM(t) in phase 2u, SOFT(t) in phase 2u+1;
+    // group B one phase later.  Both run 2n + 2 phases, n = te - tb.
+    const int n = te - tb;
     auto sync = [&](int phi) {
         __builtin_amdgcn_sched_barrier(0);
         if ((phi & 1) == 0) {
-            const int t = phi >> 1;
-            if (t + 1 < ntiles) wait_vmcnt<PP_LOADS>();   // tile t landed, tile t+1 may still fly
+            if ((phi >> 1) + 1 < n) wait_vmcnt<PP_LOADS>();   // this tile landed, the next may still fly
             else wait_vmcnt<0>();
             __builtin_amdgcn_s_barrier();
             asm volatile("" ::: "memory");
@@ -355,25 +401,25 @@ __global__ __launch_bounds__(PP_THREADS) void attn_pp_kernel(const AttnParams p)
         }
         __builtin_amdgcn_sched_barrier(0);
     };
-    load_tile(0);
-    if (ntiles > 1) load_tile(1);
+    load_tile(tb);
+    if (n > 1) load_tile(tb + 1);
     // One use of the Q fragments here, on every path: the compiler puts its wait
-    // for their loads (which also covers tiles 0 and 1, issued after them) at
-    // this point, and none in the loops below -- otherwise a path that reaches
-    // a loop without having used them makes it wait for every load in flight at
-    // the first product of each step.
+    // for their loads (which also covers the first two tiles, issued after them)
+    // at this point, and none in the loops below -- otherwise a path that
+    // reaches a loop without having used them makes it wait for every load in
+    // flight at the first product of each step.
 #pragma unroll
     for (int ks = 0; ks < D / 16; ++ks) asm volatile("" ::"v"(qf[ks]));
     const bool act = wave_active;
-    auto next = [&](int t) { return t + 2 < ntiles ? t + 2 : -1; };   // tile issued in phase 2t
+    auto next = [&](int t) { return t + 2 < te ? t + 2 : -1; };   // tile issued in tile t's GEMM phase
     if (gw == 0) {
         sync(0);
-        if (act) { __builtin_amdgcn_s_setprio(1); gemm_s(0); __builtin_amdgcn_s_setprio(0); }
-        if (next(0) >= 0) load_tile(next(0));
+        if (act) { __builtin_amdgcn_s_setprio(1); gemm_s(tb); __builtin_amdgcn_s_setprio(0); }
+        if (next(tb) >= 0) load_tile(next(tb));
         sync(1);
-        if (act) soft(std::false_type{}, 0, TileSrc{});
-        for (int t = 1; t < ntiles; ++t) {
-            sync(2 * t);
+        if (act) soft(std::false_type{}, tb, TileSrc{});
+        for (int t = tb + 1; t < te; ++t) {
+            sync(2 * (t - tb));
             const TileSrc f = plan(next(t));
             if (act) {
                 __builtin_amdgcn_s_setprio(1);
@@ -383,19 +429,19 @@ __global__ __launch_bounds__(PP_THREADS) void attn_pp_kernel(const AttnParams p)
 #pragma unroll
                 for (int q = 0; q < PP_LOADS; ++q) dma_fast(f, q);
             }
-            sync(2 * t + 1);
+            sync(2 * (t - tb) + 1);
             if (act) soft(std::false_type{}, t, TileSrc{});
         }
-        sync(2 * ntiles);
-        if (act) { __builtin_amdgcn_s_setprio(1); gemm_pv(ntiles); __builtin_amdgcn_s_setprio(0); }
-        sync(2 * ntiles + 1);
+        sync(2 * n);
+        if (act) { __builtin_amdgcn_s_setprio(1); gemm_pv(te); __builtin_amdgcn_s_setprio(0); }
+        sync(2 * n + 1);
     } else {
         sync(0);
-        if (next(0) >= 0) load_tile(next(0));
+        if (next(tb) >= 0) load_tile(next(tb));
         sync(1);
-        if (act) { __builtin_amdgcn_s_setprio(1); gemm_s(0); __builtin_amdgcn_s_setprio(0); }
-        for (int t = 1; t < ntiles; ++t) {
-            sync(2 * t);
+        if (act) { __builtin_amdgcn_s_setprio(1); gemm_s(tb); __builtin_amdgcn_s_setprio(0); }
+        for (int t = tb + 1; t < te; ++t) {
+            sync(2 * (t - tb));
             const TileSrc f = plan(next(t));
             if (act) {
                 soft(std::true_type{}, t - 1, f);
@@ -403,17 +449,17 @@ __global__ __launch_bounds__(PP_THREADS) void attn_pp_kernel(const AttnParams p)
 #pragma unroll
                 for (int q = 0; q < PP_LOADS; ++q) dma_fast(f, q);
             }
-            sync(2 * t + 1);
+            sync(2 * (t - tb) + 1);
             if (act) {
                 __builtin_amdgcn_s_setprio(1);
                 gemm(std::false_type{}, t, TileSrc{});
                 __builtin_amdgcn_s_setprio(0);
             }
         }
-        sync(2 * ntiles);
-        if (act) soft(std::false_type{}, ntiles - 1, TileSrc{});
-        sync(2 * ntiles + 1);
-        if (act) { __builtin_amdgcn_s_setprio(1); gemm_pv(ntiles); __builtin_amdgcn_s_setprio(0); }
+        sync(2 * n);
+        if (act) soft(std::false_type{}, te - 1, TileSrc{});
+        sync(2 * n + 1);
+        if (act) { __builtin_amdgcn_s_setprio(1); gemm_pv(te); __builtin_amdgcn_s_setprio(0); }
     }
 
     // ---- epilogue.  Every tile has landed and the ring is only read from here
@@ -446,6 +492,27 @@ __global__ __launch_bounds__(PP_THREADS) void attn_pp_kernel(const AttnParams p)
             for (int u = 0; u < 4; ++u)
                 if (base + u * A_THREADS < n_copy) *dp[u] = v[u];
         }
+    }
+    // Readers, a split tile: each row's unnormalised O and its (m, l) go to the
+    // workspace for the merge kernel, straight from registers (records numbered
+    // from the first row of tile tail_tile0, split-major as the merge reads them).
+    if constexpr (MODE == kModeReaders) if (nsplit > 1) {
+        const float l_row = pair_sum(rs.l);
+        if (valid) {
+            const int64_t rows_m = p.rows_total;
+            const int64_t mr = (int64_t)G * (tok0 - p.seg_tok0[0]) - (int64_t)p.tail_tile0 * kRowsPP + r;
+            const int64_t rec = ((int64_t)split * p.n_kv_heads + g) * rows_m + mr;
+            float *orow = p.ws + rec * D;
+#pragma unroll
+            for (int mt = 0; mt < D / 32; ++mt)
+#pragma unroll
+                for (int q4 = 0; q4 < 4; ++q4)
+                    *(float4 *)(orow + 32 * mt + 8 * q4 + 4 * grp) =
+                        make_float4(rs.o[mt][4 * q4], rs.o[mt][4 * q4 + 1], rs.o[mt][4 * q4 + 2], rs.o[mt][4 * q4 + 3]);
+            if (grp == 0)
+                *(float2 *)(p.ws + (int64_t)nsplit * p.n_kv_heads * rows_m * D + rec * 2) = make_float2(rs.m, l_row);
+        }
+        return;
     }
     // after this barrier no wave reads the ring any more
     __syncthreads();

@@ -23,6 +23,21 @@ constexpr int64_t kTargetWorkgroupsCont = 256;   // split-K-in-workgroup kernel:
 constexpr int64_t kMinSplitKeys = 256;
 // longest key range per workgroup for which the row-split continuation is used
 constexpr int64_t kRowsSplitMaxKeys = 640;
+// Many readers on the two-group kernel (one 128 KB workgroup per CU): tiles
+// past the last full round of workgroups are split over the keys, into at
+// most this many splits of at least kReaderMinSplitTiles key tiles each.
+// Costs in units of one whole workgroup, whose time is about kReaderTileUs per
+// key tile: a split workgroup takes 1/ns of it plus kReaderSplitFixed (its own
+// query rows, first tiles and epilogue); a split launch adds the merge launch,
+// kReaderMergeCost, and the fp32 partials written and read back at about
+// kPartialBytesPerUs.
+constexpr int64_t kCus = 256;
+constexpr int64_t kReaderMaxSplits = 16;
+constexpr int64_t kReaderMinSplitTiles = 4;
+constexpr double kReaderSplitFixed = 0.07;
+constexpr double kReaderMergeCost = 0.04;
+constexpr double kReaderTileUs = 2.0;
+constexpr double kPartialBytesPerUs = 5.0e6;
 
 // bf16 and fp16 share the 16-bit MFMA path; f16() picks the element format
 bool is16(const kvr_desc *d) { return d->dtype == KVR_BF16 || d->dtype == KVR_F16; }
@@ -104,6 +119,54 @@ Split plan_split(const kvr_desc *d, int64_t L_prefix, int64_t S) {
     return s;
 }
 
+// Many readers (n >= 2) on the two-group kernel, one launch (n <= kMaxSegments):
+// the rows of all readers are packed into tiles of kRowsPP rows, tiles per kv
+// head = ceil(G total_S / kRowsPP).  The workgroups run in rounds of kCus (one
+// per CU); the tiles of a last, partial round would leave CUs idle, so each
+// of them runs as nsplit workgroups over equal shares of its key tiles,
+// followed by the merge of their partials, nsplit chosen by the cost of the
+// rounds the split workgroups take.  A pure function of the shape,
+// non-decreasing in L_prefix.
+struct ReaderPlan {
+    int64_t tiles, tail0, nsplit, rows_tail;
+    size_t ws_bytes;
+};
+ReaderPlan plan_readers(const kvr_desc *d, int64_t L_prefix, int64_t total_S, int32_t n) {
+    const int64_t G = d->n_q_heads / d->n_kv_heads;
+    ReaderPlan r{0, 0, 1, 0, 0};
+    r.tiles = (G * total_S + kRowsPP - 1) / kRowsPP;
+    r.tail0 = r.tiles;
+    // partial-tile records are whole tokens only when G divides the tile
+    if (!use_pp(d) || n < 2 || n > kMaxSegments || kRowsPP % G != 0 || r.tiles == 0) return r;
+    const int64_t per_round = kCus / d->n_kv_heads;
+    if (per_round < 1) return r;
+    const int64_t tail = r.tiles % per_round;
+    if (tail == 0) return r;
+    const int64_t tail_wg = tail * d->n_kv_heads;
+    const int64_t rows_tail = G * total_S - (r.tiles - tail) * kRowsPP;
+    const int64_t by_keys = L_prefix / (kReaderMinSplitTiles * kKeyTile);
+    // one whole workgroup: the prefix's key tiles and a few of its own
+    const double wg_us = kReaderTileUs * (double)(L_prefix / kKeyTile + 2);
+    const double rec_bytes = (double)d->n_kv_heads * (double)rows_tail * (d->head_dim + 2) * sizeof(float);
+    int64_t ns = 1;
+    double best = 1.0 + kReaderSplitFixed;   // the tail as whole workgroups: one round
+    for (int64_t k = 2; k <= kReaderMaxSplits && k <= by_keys; ++k) {
+        const int64_t rounds = (tail_wg * k + kCus - 1) / kCus;
+        const double traffic = 2.0 * (double)k * rec_bytes / kPartialBytesPerUs / wg_us;
+        const double c = (double)rounds * (1.0 / (double)k + kReaderSplitFixed) + kReaderMergeCost + traffic;
+        if (c < best - 1e-9) {
+            best = c;
+            ns = k;
+        }
+    }
+    if (ns < 2) return r;
+    r.nsplit = ns;
+    r.tail0 = r.tiles - tail;
+    r.rows_tail = rows_tail;
+    r.ws_bytes = (size_t)ns * d->n_kv_heads * r.rows_tail * (d->head_dim + 2) * sizeof(float);
+    return r;
+}
+
 int to_status(hipError_t e) { return e == hipSuccess ? KVR_OK : KVR_ERR_DEVICE; }
 
 void fill_common(AttnParams &p, const kvr_desc *d) {
@@ -129,8 +192,9 @@ int check_rope(const kvr_rope *r, int64_t n_pos_needed) {
 
 size_t align256(size_t b) { return (b + 255) / 256 * 256; }
 
-// Workspace of the RoPE continuations: the plain split partials, then the
-// rotated query rows (single continuation only), then the rotated key rows.
+// Workspace of the RoPE continuations: the plain split partials (of a single
+// continuation, or of the many readers' split tiles), then the rotated query
+// rows (single continuation only), then the rotated key rows.
 struct RopeWs {
     size_t split, q_off, k_off, total;
 };
@@ -141,6 +205,9 @@ RopeWs rope_ws(const kvr_desc *d, int64_t L_prefix, int64_t total_S, int32_t n) 
         w.split = align256(plan_split(d, L_prefix, total_S).ws_bytes);
         w.q_off = w.split;
         w.k_off = w.q_off + align256((size_t)total_S * d->n_q_heads * row);
+    } else {
+        w.split = align256(plan_readers(d, L_prefix, total_S, n).ws_bytes);
+        w.q_off = w.k_off = w.split;
     }
     w.total = w.k_off + align256((size_t)total_S * d->n_kv_heads * row);
     return w;
@@ -300,12 +367,14 @@ int check_batched(const kvr_desc *desc, const void *Qs, const void *Ks, const vo
     return KVR_OK;
 }
 
-// rope != NULL: the query rows are rotated in registers (Ks already rotated)
+// rope != NULL: the query rows are rotated in registers (Ks already rotated).
+// ws: the split partials of plan_readers (unused when it does not split).
 int batched_impl(const kvr_desc *desc, const void *Qs, const void *Ks, const void *Vs, const int32_t *cu,
                  int32_t n, const void *kcache, const void *vcache, int64_t L_prefix, void *out,
-                 const float *rope, void *stream) {
+                 const float *rope, void *ws, void *stream) {
     const int64_t G = desc->n_q_heads / desc->n_kv_heads;
-    const int rpt = use_pp(desc) ? kRowsPP : rows_per_tile(desc);
+    const bool pp = use_pp(desc);
+    const int rpt = pp ? kRowsPP : rows_per_tile(desc);
     for (int32_t first = 0; first < n; first += kMaxSegments) {
         const int32_t cnt = (n - first) < kMaxSegments ? (n - first) : kMaxSegments;
         AttnParams p;
@@ -327,13 +396,40 @@ int batched_impl(const kvr_desc *desc, const void *Qs, const void *Ks, const voi
         if (seg == 0) continue;
         p.seg_tile0[seg] = tiles;
         p.n_seg = seg;
-        p.tiles_total = tiles;
         p.rows_total = 0;
-        const int64_t grid = (int64_t)tiles * p.n_kv_heads;
-        hipError_t e = use_pp(desc) ? launch_attn_pp(p, kModeReaders, f16(desc), (int)grid, (hipStream_t)stream)
-                       : is16(desc) ? launch_attn_bf16(p, desc->head_dim, kModeReaders, f16(desc), (int)grid,
-                                                       (hipStream_t)stream)
-                                    : launch_attn_f32(p, desc->head_dim, (int)grid, (hipStream_t)stream);
+        hipError_t e;
+        if (pp) {
+            // packed tiles; one launch (n <= kMaxSegments) may split its last round
+            const int64_t n_tok = (int64_t)p.seg_tok0[seg] - p.seg_tok0[0];
+            const ReaderPlan rp = n <= kMaxSegments ? plan_readers(desc, L_prefix, n_tok, n)
+                                                    : plan_readers(desc, 0, n_tok, 0);
+            p.tiles_total = (int32_t)rp.tiles;
+            p.tail_tile0 = (int32_t)rp.tail0;
+            p.nsplit = (int32_t)rp.nsplit;
+            p.rows_total = (int32_t)rp.rows_tail;
+            p.ws = (float *)ws;
+            const int64_t grid = (rp.tail0 + (rp.tiles - rp.tail0) * rp.nsplit) * p.n_kv_heads;
+            e = launch_attn_pp(p, kModeReaders, f16(desc), (int)grid, (hipStream_t)stream);
+            if (e == hipSuccess && rp.nsplit > 1) {
+                MergeParams mp;
+                mp.ws = (const float *)ws;
+                mp.out = (unsigned char *)out +
+                         ((int64_t)p.seg_tok0[0] + rp.tail0 * kRowsPP / G) * desc->n_q_heads * desc->head_dim *
+                             elt_bytes(desc);
+                mp.nsplit = (int32_t)rp.nsplit;
+                mp.n_q_heads = desc->n_q_heads;
+                mp.n_kv_heads = desc->n_kv_heads;
+                mp.group = (int32_t)G;
+                mp.rows = (int32_t)rp.rows_tail;
+                e = launch_merge_bf16(mp, desc->head_dim, f16(desc), (hipStream_t)stream);
+            }
+        } else {
+            p.tiles_total = tiles;
+            const int64_t grid = (int64_t)tiles * p.n_kv_heads;
+            e = is16(desc) ? launch_attn_bf16(p, desc->head_dim, kModeReaders, f16(desc), (int)grid,
+                                              (hipStream_t)stream)
+                           : launch_attn_f32(p, desc->head_dim, (int)grid, (hipStream_t)stream);
+        }
         if (e != hipSuccess) return KVR_ERR_DEVICE;
     }
     return KVR_OK;
@@ -428,7 +524,7 @@ const char *kvr_strerror(int status) {
 
 size_t kvr_workspace_bytes(const kvr_desc *desc, int64_t L_prefix, int64_t total_S, int32_t n) {
     if (check_desc(desc) != KVR_OK || L_prefix < 0 || total_S < 0 || n < 0) return (size_t)-1;
-    if (n >= 2) return 0;   // many readers: no key split, one workgroup per (reader tile, kv head)
+    if (n >= 2) return plan_readers(desc, L_prefix, total_S, n).ws_bytes;   // many readers
     return plan_split(desc, L_prefix, total_S).ws_bytes;
 }
 
@@ -553,11 +649,14 @@ int kvr_continue_q8(const kvr_desc *desc, const void *Qs, const void *Ks, const 
 int kvr_continue_batched(const kvr_desc *desc, const void *Qs, const void *Ks, const void *Vs,
                          const int32_t *cu, int32_t n, const void *kcache, const void *vcache,
                          int64_t L_prefix, void *out, void *ws, size_t ws_bytes, void *stream) {
-    (void)ws; (void)ws_bytes;   // the batched path needs no workspace
     int64_t total, longest;
     const int st = check_batched(desc, Qs, Ks, Vs, cu, n, kcache, vcache, L_prefix, out, &total, &longest);
     if (st || total == 0) return st;
-    return batched_impl(desc, Qs, Ks, Vs, cu, n, kcache, vcache, L_prefix, out, nullptr, stream);
+    const size_t need = plan_readers(desc, L_prefix, total, n).ws_bytes;
+    if (ws_bytes < need) return KVR_ERR_WORKSPACE;
+    if (need > 0 && !ws) return KVR_ERR_NULL;
+    if (!aligned16(ws)) return KVR_ERR_ALIGN;
+    return batched_impl(desc, Qs, Ks, Vs, cu, n, kcache, vcache, L_prefix, out, nullptr, ws, stream);
 }
 
 int kvr_cache_append(const kvr_desc *desc, const void *Ks, const void *Vs, int64_t S, void *kcache,
@@ -698,7 +797,7 @@ int kvr_continue_batched_rope(const kvr_desc *desc, const kvr_rope *rope, const 
         rp.job[0].n_heads = desc->n_kv_heads;
         if (launch_rope(rp, desc->head_dim, desc->dtype, (hipStream_t)stream) != hipSuccess) return KVR_ERR_DEVICE;
     }
-    return batched_impl(desc, Qs, kr, Vs, cu, n, kcache, vcache, L_prefix, out, rope->cos_sin, stream);
+    return batched_impl(desc, Qs, kr, Vs, cu, n, kcache, vcache, L_prefix, out, rope->cos_sin, ws, stream);
 }
 
 }  // extern "C"

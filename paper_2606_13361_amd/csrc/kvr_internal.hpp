@@ -49,9 +49,13 @@ struct AttnParams {
     int32_t n_seg;      // segments (independent readers); 1 for prefill / continue
     int32_t reverse;    // fp32 path: visit row tiles last-first (longest causal rows first)
     int32_t tiles_total;
-    int32_t rows_total;  // rows per kv head (partials indexing, single segment)
+    int32_t rows_total;  // rows per kv head of the split partials (from the first split row)
+    // many readers on the two-group kernel: row tiles from this one on run as
+    // nsplit key splits each (tiles_total: none)
+    int32_t tail_tile0;
     int32_t seg_tok0[kMaxSegments + 1];   // packed token offset of each segment (cu_seqlens)
-    int32_t seg_tile0[kMaxSegments + 1];  // first row tile of each segment (prefix sums)
+    int32_t seg_tile0[kMaxSegments + 1];  // first row tile of each segment (prefix sums; not used
+                                          // by the two-group kernel, whose reader tiles are packed)
 };
 
 struct AppendParams {

@@ -175,7 +175,6 @@ def test_workspace_bytes_is_a_pure_plan(lib):
     assert f(100, 24) == 0                     # short prefix: one split
     assert f(32768, 24) > f(4096, 24) > 0      # longer prefix: more splits
     assert f(32768, 24) == f(32768, 24)        # deterministic
-    assert f(32768, 24, 64) == 0               # many readers: never split
     assert f(32768, 1) % (8 * 4 * (128 + 2) * 4) == 0   # whole partial rows of fp32
     assert f(32768, 24, 1, desc(dtype=kvr.KVR_F32, capacity=1 << 16)) == 0
     assert f(-1, 3) == ctypes.c_size_t(-1).value
@@ -183,6 +182,50 @@ def test_workspace_bytes_is_a_pure_plan(lib):
     for S in (1, 24, 100):
         sizes = [f(L, S) for L in range(0, 40000, 97)]
         assert all(a <= b for a, b in zip(sizes, sizes[1:])), S
+
+
+def test_readers_workspace_plan(lib):
+    """Many readers (n >= 2) on the two-group kernel: rows packed across
+    readers into tiles of 256, 8 kv heads -> 32 tiles per round of 256
+    workgroups; the tiles of a last partial round split over the keys into the
+    ns <= min(16, L_prefix // 256) parts whose rounds cost least (a split
+    workgroup: 1/ns + 0.07 of a whole one of 2 us per key tile; the merge
+    launch: 0.04; the fp32 (O, m, l) records written and read back at 5 TB/s)."""
+    d = desc(capacity=1 << 16)
+    f = lambda Lp, S, n, dd=d: lib.kvr_workspace_bytes(ctypes.byref(dd), Lp, S, n)
+    # 64 readers, 8424 tokens over 3774: 132 tiles, 4 in the last round -> 8 splits
+    # of the 8424 * 4 - 128 * 256 = 928 rows per kv head from tile 128 on
+    assert f(3774, 8424, 64) == 8 * 8 * 928 * (128 + 2) * 4
+    # 3 readers, 301 tokens over 3774: 5 tiles, all split 6 ways
+    assert f(3774, 301, 3) == 6 * 8 * 1204 * (128 + 2) * 4
+    # 16 readers, 2058 tokens: 33 tiles, one in the last round -> 14 splits (the
+    # most with four key tiles each) of 8232 - 32 * 256 = 40 rows
+    assert f(3774, 2058, 16) == 14 * 8 * 40 * (128 + 2) * 4
+    # 8 readers, 1391 tokens: 22 tiles, one partial round of 176 workgroups; 4
+    # splits would take 3 rounds (0.96) but 185 MB of records (0.31): whole
+    assert f(3774, 1391, 8) == 0
+    assert f(3774, 8192, 64) == 0              # 128 tiles: four full rounds
+    assert f(3774, 6000, 64) == 0              # 94 tiles: 30 in the last round
+    assert f(511, 301, 3) == 0                 # fewer than 2 x 4 key tiles per split
+    assert f(512, 301, 3) == 2 * 8 * 1204 * (128 + 2) * 4
+    assert f(3774, 8424, 129) == 0             # more than one launch: no split
+    assert f(3774, 8424, 64, desc(n_q_heads=24, capacity=1 << 16)) == 0   # G = 3
+    assert f(3774, 8424, 64, desc(head_dim=64, capacity=1 << 16)) == 0    # other kernel
+    assert f(3774, 8424, 64, desc(dtype=kvr.KVR_F32, capacity=1 << 16)) == 0
+    sizes = [f(L, 301, 3) for L in range(0, 5000, 37)]
+    assert all(a <= b for a, b in zip(sizes, sizes[1:]))
+    # the batched call checks the workspace the plan needs
+    need = f(3774, 301, 3)
+    cu = [0, 24, 224, 301]
+    arr = (ctypes.c_int32 * 4)(*cu)
+    call = lambda ws, wsb: lib.kvr_continue_batched(ctypes.byref(d), A, A, A, arr, 3, A, A, 3774, A, ws, wsb, None)
+    assert call(A, need - 1) == kvr.KVR_ERR_WORKSPACE
+    assert call(None, need) == kvr.KVR_ERR_NULL
+    assert call(MIS, need) == kvr.KVR_ERR_ALIGN
+    # with RoPE: the partials, then the rotated keys
+    rot = 301 * 8 * 128 * 2
+    assert lib.kvr_workspace_bytes_rope(ctypes.byref(d), 3774, 301, 3) == (need + 255) // 256 * 256 + \
+        (rot + 255) // 256 * 256
 
 
 def test_append_errors(lib):

@@ -71,7 +71,7 @@ def test_readers_beyond_one_launch(Hq, Hkv, D, dt):
     kc, vc, d = prefill(sh, qp, kp, vp, Lp)
     qd, kd, vd = dev(qs, ks, vs)
     out = torch.full_like(qd, float("nan"))
-    kvr.kvr_continue_batched(d, qd, kd, vd, cu, kc, vc, Lp, out)
+    kvr.kvr_continue_batched(d, qd, kd, vd, cu, kc, vc, Lp, out, kvr.workspace_for(d, Lp, cu[-1], n))
     torch.cuda.synchronize()
     assert not torch.isnan(out).any()                   # every row of every reader written
     kc_o, vc_o = kp.transpose(0, 1).contiguous(), vp.transpose(0, 1).contiguous()

@@ -117,7 +117,7 @@ def test_readers_and_decode_f16():
     _, kc, vc, d = prefill(sh, qp, kp, vp, cap=Lp + 8)
     qd, kd, vd = dev(qs, ks, vs)
     out = torch.empty_like(qd)
-    kvr.kvr_continue_batched(d, qd, kd, vd, cu, kc, vc, Lp, out)
+    kvr.kvr_continue_batched(d, qd, kd, vd, cu, kc, vc, Lp, out, kvr.workspace_for(d, Lp, cu[-1], len(lens)))
     torch.cuda.synchronize()
     kc_o, vc_o = kp.transpose(0, 1).contiguous(), vp.transpose(0, 1).contiguous()
     for r in range(len(lens)):

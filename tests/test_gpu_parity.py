@@ -278,7 +278,7 @@ def test_many_readers_batched():
     _, kc, vc, d = gpu_prefill(sh, qp, kp, vp, capacity=Lp)
     qd, kd, vd = dev(qs, ks, vs)
     out = torch.empty_like(qd)
-    kvr.kvr_continue_batched(d, qd, kd, vd, cu, kc, vc, Lp, out)
+    kvr.kvr_continue_batched(d, qd, kd, vd, cu, kc, vc, Lp, out, kvr.workspace_for(d, Lp, total, len(lens)))
     torch.cuda.synchronize()
     got = out.cpu()
     kc_o, vc_o = kp.transpose(0, 1).contiguous(), vp.transpose(0, 1).contiguous()

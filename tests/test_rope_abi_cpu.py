@@ -110,7 +110,9 @@ def test_workspace_bytes(lib, dtype, elt):
     for Lp, S in ((0, 24), (4096, 24), (32768, 1), (32768, 300)):
         # the plain split partials, then rotated Q rows and rotated K rows
         assert f(Lp, S) == up(g(Lp, S)) + up(S * 32 * 128 * elt) + up(S * 8 * 128 * elt)
-    assert f(3774, 8424, 64) == up(8424 * 8 * 128 * elt)       # readers: rotated keys only
+    # readers: the split partials of their last tiles (bf16 / fp16), then the rotated keys
+    assert f(3774, 8424, 64) == up(g(3774, 8424, 64)) + up(8424 * 8 * 128 * elt)
+    assert (g(3774, 8424, 64) > 0) == (dtype != kvr.KVR_F32)
     assert f(-1, 3) == SZ_MAX
     sizes = [f(L, 24) for L in range(0, 40000, 211)]
     assert all(a <= b for a, b in zip(sizes, sizes[1:]))
