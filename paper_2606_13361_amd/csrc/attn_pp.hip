@@ -80,7 +80,7 @@ __global__ __launch_bounds__(PP_THREADS) void attn_pp_kernel(const AttnParams p)
     const int G = p.group;
     const int g = blockIdx.x % p.n_kv_heads;
     const int bh = blockIdx.x / p.n_kv_heads;
-    int tile_lin, split = 0, nsplit = 1, tok0, R, row0;
+    int tile_lin, split = 0, nsplit = 1, tok0, R, row0, seg0 = 0;
     if constexpr (MODE == kModePrefill) {
         tile_lin = p.tiles_total - 1 - bh;
         tok0 = 0;
@@ -96,7 +96,8 @@ __global__ __launch_bounds__(PP_THREADS) void attn_pp_kernel(const AttnParams p)
         }
         const int T0 = p.seg_tok0[0];
         const int prow0 = tile_lin * kRowsPP;                 // packed row of the launch
-        tok0 = p.seg_tok0[segment_of_token(p, T0 + prow0 / G, 0)];
+        seg0 = segment_of_token(p, T0 + prow0 / G, 0);
+        tok0 = p.seg_tok0[seg0];
         R = G * (p.seg_tok0[p.n_seg] - tok0);
         row0 = prow0 - G * (tok0 - T0);
     }
@@ -122,13 +123,18 @@ __global__ __launch_bounds__(PP_THREADS) void attn_pp_kernel(const AttnParams p)
     // reader), the wave's largest lo, and the row's own position for RoPE
     int lo = npre, hole_end = npre;
     if constexpr (MODE == kModeReaders) {
+        // the readers that start inside the tile, by a uniform scan (scalar
+        // loads; none for a tile inside one reader): the lane keeps the last
+        // start at or before its token
         const int t_abs = tok0 + tok;
-        lo = npre + (p.seg_tok0[segment_of_token(p, t_abs, 0)] - tok0);
-        if (!valid) lo = npre;
-        int m = lo;
-#pragma unroll
-        for (int x = 1; x < 64; x <<= 1) m = max(m, __shfl_xor(m, x));
-        hole_end = __builtin_amdgcn_readfirstlane(m);
+        const int t_last = tok0 + row_last / G;
+        int lo_tok = tok0;
+        for (int k = seg0 + 1; k < p.n_seg && p.seg_tok0[k] <= t_last; ++k)
+            lo_tok = t_abs >= p.seg_tok0[k] ? p.seg_tok0[k] : lo_tok;
+        lo = valid ? npre + (lo_tok - tok0) : npre;
+        // rows (and their readers) increase with the lane: the wave's largest lo
+        // is its last valid row's
+        if (wave_active) hole_end = __builtin_amdgcn_readlane(lo, min(31, R - 1 - wrow0));
     }
     const int rope_pos = pos - (lo - npre);
 
