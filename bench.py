@@ -787,9 +787,10 @@ def model_table1(torch, A, W, dev, lengths=(255, 485, 945, 1888, 3774)):
         })
     res = {
         "what": "random-weight Qwen3-4B-shaped model, bf16, 36 layers (RMSNorm, QKV / O / gate-up / down "
-                "products on hipBLASLt, q/k norm + RoPE, this library's attention), tied 151936-row output "
-                "embedding: full prefill of the context (last row's logits) vs one continuation step of one "
-                "token over the resident caches (its logits); medians of 5 prefills and 20 steps",
+                "products, q/k norm + RoPE, this library's attention), tied 151936-row output embedding: "
+                "full prefill of the context (last row's logits; products on hipBLASLt) vs one continuation "
+                "step of one token over the resident caches (its logits; the library's one-row product "
+                "kernels with the norms and the activation fused); medians of 5 prefills and 20 steps",
         "weights_GB": round(weight_bytes / 1e9, 3),
         "rows": rows,
         "paper_context": "paper Table 1: Qwen3-4B fp16 on Apple M1 Pro (MPS), speedup 8.6-49.7x; the speedup "

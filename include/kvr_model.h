@@ -24,9 +24,10 @@
  * the host before any launch, work enqueued on `stream`, 16-byte alignment).
  * Elements are bf16 or fp16 (desc->dtype); every activation is held in that
  * format between operations and computed in fp32.  Weights are row-major
- * [out][in] (the layout of a linear layer's weight).  Matrix products run on
- * hipBLASLt (fp32 accumulation); the other operations are this library's
- * kernels.
+ * [out][in] (the layout of a linear layer's weight).  Matrix products of more
+ * than one token run on hipBLASLt (fp32 accumulation); a one-token step's
+ * products, and every other operation, are this library's kernels (fp32
+ * accumulation; the step's RMSNorms and SiLU gate run inside its products).
  */
 #ifndef KVR_MODEL_H
 #define KVR_MODEL_H
