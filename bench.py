@@ -52,6 +52,8 @@ def parse():
     ap.add_argument("--no-artifact", action="store_true")
     ap.add_argument("--no-rope", action="store_true")
     ap.add_argument("--no-readers-sweep", action="store_true")
+    ap.add_argument("--readers-sweep-only", action="store_true",
+                    help="only the 2..64-reader sweep (one JSON object)")
     ap.add_argument("--no-model", action="store_true",
                     help="skip the random-weight 36-layer model (Table 1's prefill vs continuation step)")
     ap.add_argument("--model-only", action="store_true")
@@ -160,6 +162,10 @@ def main():
 
     if args.model_only:
         print(json.dumps({"model": model_table1(torch, A, W, dev)}), flush=True)
+        return
+
+    if args.readers_sweep_only:
+        print(json.dumps({"readers_sweep": readers_sweep(torch, kvr, A, W, dev, stream)}), flush=True)
         return
 
     if args.sweep_only:
