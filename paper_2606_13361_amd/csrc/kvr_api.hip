@@ -352,11 +352,19 @@ int check_batched(const kvr_desc *desc, const void *Qs, const void *Ks, const vo
     for (int32_t i = 0; i < n; ++i)
         if (cu[i + 1] < cu[i]) return KVR_ERR_SHAPE;
     if ((int64_t)cu[n] > kMaxTokens) return KVR_ERR_SHAPE;
+    const int64_t G = desc->n_q_heads / desc->n_kv_heads;
     for (int32_t i = 0; i < n; ++i) {
         const int64_t len = cu[i + 1] - cu[i];
-        if ((int64_t)(desc->n_q_heads / desc->n_kv_heads) * len > 0x7fffffff) return KVR_ERR_SHAPE;
+        if (G * len > 0x7fffffff) return KVR_ERR_SHAPE;
         if (len > *longest) *longest = len;
     }
+    // the two-group kernel packs the rows of a launch's readers: row indices
+    // of a whole launch group must fit 32 bits there
+    if (use_pp(desc))
+        for (int32_t first = 0; first < n; first += kMaxSegments) {
+            const int32_t last = (n - first) < kMaxSegments ? n : first + kMaxSegments;
+            if (G * ((int64_t)cu[last] - cu[first]) > 0x7fffffff) return KVR_ERR_SHAPE;
+        }
     if (cu[n] == 0) return KVR_OK;
     if (!Qs || !Ks || !Vs || !out) return KVR_ERR_NULL;
     if (L_prefix > 0 && (!kcache || !vcache)) return KVR_ERR_NULL;

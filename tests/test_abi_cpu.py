@@ -249,6 +249,12 @@ def test_batched_errors(lib):
     assert lib.kvr_continue_batched(ctypes.byref(d), A, A, A, None, 2, A, A, 4, A, None, 0, None) == kvr.KVR_ERR_NULL
     assert batched(lib, d, [0, 4], out=MIS) == kvr.KVR_ERR_ALIGN
     assert batched(lib, d, [0, 4], kc=None) == kvr.KVR_ERR_NULL
+    # packed rows of one launch (two-group kernel: bf16, d = 128) must fit 32-bit
+    # row indices even when each reader's do: G = 4096 (4096 q heads, 1 kv head)
+    big = desc(n_q_heads=4096, n_kv_heads=1, capacity=100)
+    assert batched(lib, big, [0, 300000, 600000]) == kvr.KVR_ERR_SHAPE        # 4096 x 600000 > 2^31
+    assert batched(lib, big, [0, 300000, 600000], Lp=0, Q=None) == kvr.KVR_ERR_SHAPE
+    assert batched(lib, big, [0, 200000, 400000], Q=None) == kvr.KVR_ERR_NULL  # 4096 x 400000 < 2^31
 
 
 def test_python_binding_rejects_metadata_mismatch():
