@@ -4,9 +4,10 @@ last partial round of row tiles split over the keys and merged.
 Every row of every reader against the fp64 oracle (1e-2 for 16-bit inputs),
 on shapes that put reader boundaries inside row tiles (a row of a later
 reader must not see the earlier readers' rows in its tile), readers of one
-token, empty readers, no cached prefix, group sizes 1, 3, 4 and 8 (3: rows of
-a token straddle tiles, no key split), fp16, RoPE, and batches small enough
-that every tile is split.  Each case also checks that the call was planned
+token, empty readers, no cached prefix, group sizes 1, 2, 3, 4 and 8 (3: rows
+of a token straddle tiles, no key split), fp16, RoPE (bf16 and fp16), 128
+readers in one launch and 129 in two, prefixes just at and below the split
+threshold, and batches small enough that every tile is split.  Each case also checks that the call was planned
 the way it names (split or not, from the workspace it asks for), that every
 output row was written, and that two calls give the same bits.
 """
@@ -50,6 +51,10 @@ def lengths(kind, seed):
         return [5, 1, 60, 0, 130, 1, 0, 33]
     if kind == "flat93":          # 64 readers of 93 tokens: 93 tiles, 29 in the last round
         return [93] * 64
+    if kind == "r128":            # the most readers one launch holds, 1-40 tokens each
+        return [1 + int(x) for x in torch.randint(0, 40, (128,), generator=g)]
+    if kind == "r129":            # one reader past a launch: packed per launch, never split
+        return [1 + int(x) for x in torch.randint(0, 40, (129,), generator=g)]
     if kind.startswith("u"):      # "u<n>": n readers, S ~ U[24, 256]
         return [int(x) for x in torch.randint(24, 257, (int(kind[1:]),), generator=g)]
     raise ValueError(kind)
@@ -68,6 +73,11 @@ CASES = [
     ("40 readers, a 23-tile last round kept whole", 32, 8, BF16, 2000, "u40", False),
     ("64 x 93 tokens, last round too full to split", 32, 8, BF16, 1500, "flat93", False),
     ("4 kv heads", 32, 4, BF16, 2100, "mixed", True),
+    ("128 readers, one launch", 32, 8, BF16, 1000, "r128", True),
+    ("129 readers, two launches", 32, 8, BF16, 1000, "r129", False),
+    ("G = 2, 4 kv heads", 8, 4, BF16, 900, "u6", True),
+    ("512 cached keys: two splits at most", 32, 8, BF16, 512, "three", True),
+    ("511 cached keys: too few to split", 32, 8, BF16, 511, "three", False),
 ]
 
 
@@ -116,11 +126,12 @@ def test_packed_readers_vs_oracle(name, Hq, Hkv, dt, Lp, kind, split):
     say("  max |gpu - oracle| = %.5f" % worst)
 
 
-def test_packed_readers_rope_split():
+@pytest.mark.parametrize("dt", [BF16, F16], ids=["bf16", "fp16"])
+def test_packed_readers_rope_split(dt):
     """RoPE: each reader's rows rotated at L_prefix + (token within the reader),
     not at their place in the packed tile; three readers, every tile split."""
-    say("packed readers with RoPE, split")
-    sh = W.Shape(32, 8, 128, BF16)
+    say("packed readers with RoPE, split, %s" % dt)
+    sh = W.Shape(32, 8, 128, dt)
     Lp = 2000
     lens = [24, 100, 31]
     cu = W.cu_seqlens(lens)
@@ -129,9 +140,9 @@ def test_packed_readers_rope_split():
     g = W.gen(91)
     qp, kp, vp = W.qkv(Lp, sh, generator=g)
     qs, ks, vs = W.qkv(cu[-1], sh, generator=g)
-    d = kvr.make_desc(32, 8, 128, BF16, Lp)
+    d = kvr.make_desc(32, 8, 128, dt, Lp)
     qd, kd, vd = dev(qp, kp, vp)
-    kc = torch.zeros((8, Lp, 128), dtype=BF16, device=DEV)
+    kc = torch.zeros((8, Lp, 128), dtype=dt, device=DEV)
     vc = torch.zeros_like(kc)
     kvr.kvr_prefill_rope(d, tab, qd, kd, vd, Lp, torch.empty_like(qd), kc, vc)
     assert kvr.kvr_workspace_bytes(d, Lp, cu[-1], n) > 0      # the split plan
@@ -141,12 +152,13 @@ def test_packed_readers_rope_split():
                                   kvr.workspace_for_rope(d, Lp, cu[-1], n))
     torch.cuda.synchronize()
     assert not torch.isnan(out).any()
-    k_rot = ORope.round_to(ORope.rotate(kp, np.arange(Lp), ORope.QWEN3_BASE), "bf16")
+    fmt = "fp16" if dt == F16 else "bf16"
+    k_rot = ORope.round_to(ORope.rotate(kp, np.arange(Lp), ORope.QWEN3_BASE), fmt)
     kc_o = np.transpose(k_rot, (1, 0, 2)).copy()
     vc_o = vp.transpose(0, 1).contiguous()
     for r in range(n):
         a, b = cu[r], cu[r + 1]
-        want, _, _ = ORope.continue_(qs[a:b], ks[a:b], vs[a:b], kc_o, vc_o, Lp, ORope.QWEN3_BASE, fmt="bf16")
+        want, _, _ = ORope.continue_(qs[a:b], ks[a:b], vs[a:b], kc_o, vc_o, Lp, ORope.QWEN3_BASE, fmt=fmt)
         assert maxabs(out[a:b], want) <= TOL, r
 
 
