@@ -17,11 +17,31 @@
 
 static int g_launches = 0;
 static int64_t g_nsplit = -1, g_chunk = -1;   // the split plan the last continuation launch got
+static int g_pp_bad = 0;                       // many-readers launches whose plan broke an invariant
+static int g_pp_split = 0, g_pp_whole = 0;     // many-readers launches checked: split last round or not
+static int64_t g_pp_grid = -1, g_pp_tail0 = -1, g_pp_rows = -1;
 
 namespace kvr {
 hipError_t launch_attn_bf16(const AttnParams &, int, int, bool, int, hipStream_t) { ++g_launches; return hipErrorUnknown; }
 hipError_t launch_merge_bf16(const MergeParams &, int, bool, hipStream_t) { ++g_launches; return hipErrorUnknown; }
-hipError_t launch_attn_pp(const AttnParams &, int, bool, int, hipStream_t) { ++g_launches; return hipErrorUnknown; }
+// many readers on the two-group kernel: the packed plan must cover its tiles
+// with whole workgroups (split tiles ns times), and split partial rows must
+// number the rows from the first split tile to the end of the launch
+hipError_t launch_attn_pp(const AttnParams &p, int mode, bool, int grid, hipStream_t) {
+    ++g_launches;
+    if (mode == kModeReaders) {
+        const int64_t ns = p.nsplit, tiles = p.tiles_total, t0 = p.tail_tile0;
+        const int64_t rows = (int64_t)p.group * ((int64_t)p.seg_tok0[p.n_seg] - p.seg_tok0[0]);
+        bool ok = ns >= 1 && ns <= 16 && t0 >= 0 && t0 <= tiles && tiles == (rows + kRowsPP - 1) / kRowsPP &&
+                  (int64_t)grid == (t0 + (tiles - t0) * ns) * p.n_kv_heads;
+        if (ns > 1) ok = ok && t0 < tiles && p.ws && p.rows_total == rows - t0 * kRowsPP && kRowsPP % p.group == 0;
+        else ok = ok && t0 == tiles;
+        if (!ok) ++g_pp_bad;
+        ++(ns > 1 ? g_pp_split : g_pp_whole);
+        g_pp_grid = grid; g_pp_tail0 = t0; g_pp_rows = p.rows_total;
+    }
+    return hipErrorUnknown;
+}
 hipError_t launch_attn_rows(const AttnParams &p, bool, int, hipStream_t) {
     ++g_launches; g_nsplit = p.nsplit; g_chunk = p.chunk; return hipErrorUnknown;
 }
@@ -107,6 +127,20 @@ static void fixed_cases() {
     EXPECT(kvr_continue_batched(&d, A, A, A, nullptr, 3, A, A, 100, A, A, big, nullptr), KVR_ERR_NULL);
     EXPECT(kvr_continue_batched(&d, A, A, A, cu_ok, 3, A, A, 5000, A, A, big, nullptr), KVR_ERR_CAPACITY);
     EXPECT(kvr_continue_batched(&d, A, A, A, cu_ok, 3, A, A, 100, A, A, big, nullptr), KVR_ERR_DEVICE);
+    {
+        // 64 readers, 8424 tokens over 3774: 132 tiles per kv head, the last 4 split 8 ways
+        std::vector<int32_t> cu64(65, 0);
+        const int step[4] = {120, 140, 131, 135};
+        for (int i = 1; i <= 64; ++i) cu64[i] = cu64[i - 1] + step[i % 4];
+        cu64[64] = 8424;
+        kvr_desc dr = desc(32, 8, 128, KVR_BF16, 4096);
+        const size_t wsr = kvr_workspace_bytes(&dr, 3774, 8424, 64);
+        EXPECT(wsr == (size_t)8 * 8 * 928 * 130 * 4, 1);
+        EXPECT(kvr_continue_batched(&dr, A, A, A, cu64.data(), 64, A, A, 3774, A, A, wsr - 1, nullptr),
+               KVR_ERR_WORKSPACE);
+        EXPECT(kvr_continue_batched(&dr, A, A, A, cu64.data(), 64, A, A, 3774, A, A, wsr, nullptr), KVR_ERR_DEVICE);
+        EXPECT(g_pp_grid == (128 + 4 * 8) * 8 * 1 && g_pp_tail0 == 128 && g_pp_rows == 928, 1);
+    }
     // int8 artifact
     kvr_desc f32 = desc(32, 8, 128, KVR_F32);
     EXPECT(kvr_quantize_cache(&f32, A, A, 10, A, A, (float *)A, nullptr), KVR_ERR_DTYPE);
@@ -242,10 +276,19 @@ int main() {
     fixed_cases();
     split_plans();
     fuzz();
+    if (g_pp_bad) {
+        fprintf(stderr, "%d many-readers launches broke a plan invariant\n", g_pp_bad);
+        ++fails;
+    }
+    if (g_pp_split < 20 || g_pp_whole < 20) {
+        fprintf(stderr, "only %d split and %d whole many-readers plans checked\n", g_pp_split, g_pp_whole);
+        ++fails;
+    }
     if (fails) {
         fprintf(stderr, "%d checks failed\n", fails);
         return 1;
     }
-    printf("host driver: all checks passed (%d stub launches)\n", g_launches);
+    printf("host driver: all checks passed (%d stub launches; many-readers plans: %d split, %d whole)\n", g_launches,
+           g_pp_split, g_pp_whole);
     return 0;
 }
