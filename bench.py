@@ -54,6 +54,8 @@ def parse():
     ap.add_argument("--no-readers-sweep", action="store_true")
     ap.add_argument("--readers-sweep-only", action="store_true",
                     help="only the 2..64-reader sweep (one JSON object)")
+    ap.add_argument("--decode36-only", action="store_true",
+                    help="only the 36-layer decode chain (one JSON object)")
     ap.add_argument("--no-model", action="store_true",
                     help="skip the random-weight 36-layer model (Table 1's prefill vs continuation step)")
     ap.add_argument("--model-only", action="store_true")
@@ -162,6 +164,10 @@ def main():
 
     if args.model_only:
         print(json.dumps({"model": model_table1(torch, A, W, dev)}), flush=True)
+        return
+
+    if args.decode36_only:
+        print(json.dumps({"decode36": decode36(torch, kvr, A, W, dev, stream)}), flush=True)
         return
 
     if args.readers_sweep_only:
