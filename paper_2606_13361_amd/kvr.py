@@ -211,7 +211,9 @@ def kvr_continue_append(desc, Qs, Ks, Vs, kcache, vcache, L_prefix, S, out, ws=N
 
 def kvr_continue_batched(desc, Qs, Ks, Vs, cu_seqlens, kcache, vcache, L_prefix, out, ws=None,
                          stream=None):
-    """cu_seqlens: host sequence of n+1 ints (a list or a CPU tensor)."""
+    """cu_seqlens: host sequence of n+1 ints (a list or a CPU tensor).  ws: the
+    workspace of workspace_for(desc, L_prefix, cu_seqlens[-1], n) (None when
+    that is None: the call's plan splits no row tile over the keys)."""
     Hq, Hkv, d = desc.n_q_heads, desc.n_kv_heads, desc.head_dim
     cu = [int(x) for x in (cu_seqlens.tolist() if isinstance(cu_seqlens, torch.Tensor) else cu_seqlens)]
     n = len(cu) - 1
